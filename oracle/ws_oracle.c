@@ -1,0 +1,424 @@
+/*
+ * ws_oracle.c -- plain fp64 CPU reference for block-causal attention.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path links, loads or
+ * calls this file; only the test suite, the smoke check and the benchmark's
+ * CPU-baseline leg do.  It shares no source with the GPU library.
+ *
+ * What it computes (Wan-Streamer v0.1, Abstract and Sec. 1 with Fig. 1:
+ * the interleaved token stream is coordinated by block-causal attention;
+ * Sec. 2.1, Eq. 1: the response of unit k is conditioned on every input of
+ * units <= k and every response of units < k; Sec. 2.4: the performer
+ * appends each received KV slice to a full-history cache):
+ *
+ *   a token whose block id is beta_q may see exactly the keys j whose block
+ *   id beta_k(j) is <= beta_q, i.e. its own block in both directions and
+ *   every earlier block;
+ *
+ *   o_i   = sum_{j visible} softmax_j(scale * <q_i, k_j>) v_j
+ *   lse_i = m_i + ln(sum_{j visible} exp(scale * <q_i, k_j> - m_i)),
+ *           m_i = max_{j visible} scale * <q_i, k_j>.
+ *
+ * Everything is fp64.  bf16 inputs are widened exactly (bit pattern << 16 is
+ * the fp32 value, and fp32 -> fp64 is exact).  Dot products are summed
+ * sequentially over the head dimension; the mask row is materialised
+ * explicitly for every query; masked keys never enter the max or the sums.
+ * Grouped-query attention: query head h reads KV head floor(h / G) with
+ * G = Hq / Hkv (contiguous groups).
+ *
+ * Rows are independent, so results do not depend on the thread count.
+ *
+ * Compile-time switch WSO_MUTANT (default 0) plants one deliberate mistake;
+ * it exists only so the test suite can show that its pins catch such
+ * mistakes.  A normal build never defines it.
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifndef WSO_MUTANT
+#define WSO_MUTANT 0
+#endif
+
+enum { WSO_F64 = 0, WSO_BF16 = 1 };
+
+/* A 4-d token tensor [B][L][H][d] with the last dimension contiguous;
+ * strides are in elements. */
+typedef struct {
+    const void *base;
+    int dtype;
+    int64_t sb, st, sh;
+} wso_view;
+
+static double wso_load(const wso_view *v, int64_t b, int64_t t, int64_t h, int64_t c)
+{
+    int64_t idx = b * v->sb + t * v->st + h * v->sh + c;
+    if (v->dtype == WSO_F64)
+        return ((const double *)v->base)[idx];
+    uint16_t bits = ((const uint16_t *)v->base)[idx];
+    uint32_t w = (uint32_t)bits << 16;
+    float f;
+    memcpy(&f, &w, sizeof f);
+    return (double)f;
+}
+
+/* Which kind of problem a job describes. */
+enum { WSO_PREFILL = 0, WSO_STEP = 1 };
+
+typedef struct {
+    int kind;
+    int B, Lq, Hq, Hkv, d;
+    double scale;
+    /* prefill: queries and keys are the same L tokens; offsets [B][nb+1] */
+    wso_view q, k, v;
+    const int32_t *offsets;
+    int nb;
+    /* step: keys are cache tokens [0, Lc[b]) followed by the Lq new tokens */
+    wso_view kc, vc;
+    const int32_t *cache_lens;
+    /* row list: nrows triples (b, h, i); NULL means every row */
+    const int32_t *rows;
+    int64_t nrows;
+    /* outputs */
+    double *out;   /* all rows: [B][Lq][Hq][d]; row list: [nrows][d] */
+    double *lse;   /* all rows: [B][Hq][Lq];   row list: [nrows]; may be NULL */
+    double *probs; /* optional, row list only: [nrows][Lk_max] */
+    int64_t lk_max;
+} wso_job;
+
+/* Block id of token t given the block boundaries off[0..nb]:
+ * the n with off[n] <= t < off[n+1]. */
+static int wso_block_of(const int32_t *off, int nb, int64_t t)
+{
+    for (int n = 0; n < nb; ++n) {
+#if WSO_MUTANT == 6
+        if (off[n] < t && t <= off[n + 1])
+            return n;
+#else
+        if (off[n] <= t && t < off[n + 1])
+            return n;
+#endif
+    }
+    return nb; /* past the end: later than every block */
+}
+
+/* Number of keys of stream b. */
+static int64_t wso_num_keys(const wso_job *J, int b)
+{
+    if (J->kind == WSO_PREFILL)
+        return J->Lq;
+    return (int64_t)J->cache_lens[b] + J->Lq;
+}
+
+/* Element c of key (or value) j of stream b, KV head g. */
+static double wso_key(const wso_job *J, int is_v, int b, int64_t j, int g, int c)
+{
+    if (J->kind == WSO_PREFILL)
+        return wso_load(is_v ? &J->v : &J->k, b, j, g, c);
+    int64_t lc = J->cache_lens[b];
+    if (j < lc)
+        return wso_load(is_v ? &J->vc : &J->kc, b, j, g, c);
+    return wso_load(is_v ? &J->v : &J->k, b, j - lc, g, c);
+}
+
+/* Scratch owned by one worker thread. */
+typedef struct {
+    double *s;
+    unsigned char *mask;
+    double *acc;
+} wso_scratch;
+
+/* One query row: materialise the mask row, then the softmax-weighted sum. */
+static void wso_row(const wso_job *J, wso_scratch *S, int b, int h, int64_t i,
+                    double *o, double *lse_out, double *p_out)
+{
+    const int G = J->Hq / J->Hkv;
+#if WSO_MUTANT == 3
+    const int g = h % J->Hkv;
+#else
+    const int g = h / G;
+#endif
+    const int64_t Lk = wso_num_keys(J, b);
+    const int d = J->d;
+
+    /* 1. explicit mask row from block ids */
+    int beta_q;
+    if (J->kind == WSO_PREFILL)
+        beta_q = wso_block_of(J->offsets + (int64_t)b * (J->nb + 1), J->nb, i);
+    else
+        beta_q = 1;
+    for (int64_t j = 0; j < Lk; ++j) {
+        int beta_k;
+        if (J->kind == WSO_PREFILL)
+            beta_k = wso_block_of(J->offsets + (int64_t)b * (J->nb + 1), J->nb, j);
+        else
+            beta_k = (j < J->cache_lens[b]) ? 0 : 1;
+#if WSO_MUTANT == 1
+        S->mask[j] = (unsigned char)(beta_k < beta_q);
+#elif WSO_MUTANT == 8
+        S->mask[j] = (unsigned char)(beta_k >= beta_q);
+#else
+        S->mask[j] = (unsigned char)(beta_k <= beta_q);
+#endif
+    }
+
+    /* 2. logits of visible keys, and their maximum */
+    double m = -INFINITY;
+    for (int64_t j = 0; j < Lk; ++j) {
+        if (!S->mask[j])
+            continue;
+        double dot = 0.0;
+        for (int c = 0; c < d; ++c) {
+            double qv = wso_load(&J->q, b, i, h, c);
+#if WSO_MUTANT == 4
+            double kv = wso_key(J, 0, b, (j + 1) % Lk, g, c);
+#else
+            double kv = wso_key(J, 0, b, j, g, c);
+#endif
+            dot += qv * kv;
+        }
+#if WSO_MUTANT == 2
+        S->s[j] = dot;
+#else
+        S->s[j] = J->scale * dot;
+#endif
+        if (S->s[j] > m)
+            m = S->s[j];
+    }
+
+    /* 3. unnormalised weights and their sum */
+    double l = 0.0;
+    for (int64_t j = 0; j < Lk; ++j) {
+        if (!S->mask[j]) {
+            S->s[j] = 0.0;
+            continue;
+        }
+        S->s[j] = exp(S->s[j] - m);
+        l += S->s[j];
+    }
+
+    /* 4. weighted sum of values, normalised */
+    for (int c = 0; c < d; ++c)
+        S->acc[c] = 0.0;
+    for (int64_t j = 0; j < Lk; ++j) {
+        if (!S->mask[j])
+            continue;
+        for (int c = 0; c < d; ++c)
+            S->acc[c] += S->s[j] * wso_key(J, 1, b, j, g, c);
+    }
+    for (int c = 0; c < d; ++c) {
+#if WSO_MUTANT == 7
+        o[c] = S->acc[c];
+#else
+        o[c] = S->acc[c] / l;
+#endif
+    }
+    if (lse_out) {
+#if WSO_MUTANT == 5
+        *lse_out = m;
+#else
+        *lse_out = m + log(l);
+#endif
+    }
+    if (p_out) {
+        for (int64_t j = 0; j < Lk; ++j)
+            p_out[j] = S->s[j] / l;
+    }
+}
+
+typedef struct {
+    const wso_job *J;
+    int64_t first, last; /* half-open range of row indices */
+    int status;
+} wso_task;
+
+static void *wso_worker(void *arg)
+{
+    wso_task *T = (wso_task *)arg;
+    const wso_job *J = T->J;
+    int64_t lk_cap = J->Lq;
+    if (J->kind == WSO_STEP) {
+        for (int b = 0; b < J->B; ++b)
+            if (wso_num_keys(J, b) > lk_cap)
+                lk_cap = wso_num_keys(J, b);
+    }
+    wso_scratch S;
+    S.s = (double *)malloc(sizeof(double) * (size_t)(lk_cap > 0 ? lk_cap : 1));
+    S.mask = (unsigned char *)malloc((size_t)(lk_cap > 0 ? lk_cap : 1));
+    S.acc = (double *)malloc(sizeof(double) * (size_t)J->d);
+    if (!S.s || !S.mask || !S.acc) {
+        free(S.s);
+        free(S.mask);
+        free(S.acc);
+        T->status = -1;
+        return NULL;
+    }
+    for (int64_t r = T->first; r < T->last; ++r) {
+        int b, h;
+        int64_t i;
+        double *o, *lse_out, *p_out = NULL;
+        if (J->rows) {
+            b = J->rows[3 * r + 0];
+            h = J->rows[3 * r + 1];
+            i = J->rows[3 * r + 2];
+            o = J->out + r * J->d;
+            lse_out = J->lse ? J->lse + r : NULL;
+            if (J->probs)
+                p_out = J->probs + r * J->lk_max;
+        } else {
+            /* r enumerates (b, i, h) in output order */
+            h = (int)(r % J->Hq);
+            i = (r / J->Hq) % J->Lq;
+            b = (int)(r / ((int64_t)J->Hq * J->Lq));
+            o = J->out + r * J->d;
+            lse_out = J->lse ? J->lse + ((int64_t)b * J->Hq + h) * J->Lq + i : NULL;
+        }
+        wso_row(J, &S, b, h, i, o, lse_out, p_out);
+    }
+    free(S.s);
+    free(S.mask);
+    free(S.acc);
+    T->status = 0;
+    return NULL;
+}
+
+static int wso_run(const wso_job *J, int nthreads)
+{
+    int64_t total = J->rows ? J->nrows : (int64_t)J->B * J->Lq * J->Hq;
+    if (total <= 0)
+        return 0;
+    if (nthreads < 1)
+        nthreads = 1;
+    if (nthreads > total)
+        nthreads = (int)total;
+    pthread_t *th = (pthread_t *)calloc((size_t)nthreads, sizeof(pthread_t));
+    wso_task *tasks = (wso_task *)calloc((size_t)nthreads, sizeof(wso_task));
+    if (!th || !tasks) {
+        free(th);
+        free(tasks);
+        return -1;
+    }
+    for (int t = 0; t < nthreads; ++t) {
+        tasks[t].J = J;
+        tasks[t].first = total * t / nthreads;
+        tasks[t].last = total * (t + 1) / nthreads;
+        tasks[t].status = -1;
+    }
+    int started = 0;
+    for (int t = 1; t < nthreads; ++t) {
+        if (pthread_create(&th[t], NULL, wso_worker, &tasks[t]) != 0)
+            break;
+        started = t;
+    }
+    wso_worker(&tasks[0]);
+    int rc = tasks[0].status;
+    for (int t = 1; t <= started; ++t) {
+        pthread_join(th[t], NULL);
+        if (tasks[t].status != 0)
+            rc = -1;
+    }
+    /* rows of threads that could not be started are done here */
+    for (int t = started + 1; t < nthreads; ++t) {
+        wso_worker(&tasks[t]);
+        if (tasks[t].status != 0)
+            rc = -1;
+    }
+    free(th);
+    free(tasks);
+    return rc;
+}
+
+static int wso_check_common(int B, int Lq, int Hq, int Hkv, int d)
+{
+    if (B < 0 || Lq < 0 || Hq <= 0 || Hkv <= 0 || d <= 0)
+        return -2;
+    if (Hq % Hkv != 0)
+        return -2;
+    return 0;
+}
+
+/*
+ * Whole-sequence block-causal attention.  q, k, v: [B][L][H][d] contiguous
+ * (dtype WSO_F64 or WSO_BF16 bit patterns).  offsets: [B][nb+1] block
+ * boundaries, offsets[b][0] = 0, non-decreasing, offsets[b][nb] = L.
+ * rows: NULL for every row, else nrows triples (b, h, i).  probs (row list
+ * only, may be NULL): [nrows][L] normalised attention weights.
+ * Returns 0 on success, -2 on bad arguments, -1 on allocation failure.
+ */
+int wso_prefill(const void *q, const void *k, const void *v, int dtype,
+                int B, int L, int Hq, int Hkv, int d,
+                const int32_t *offsets, int nb, double scale,
+                const int32_t *rows, int64_t nrows,
+                double *out, double *lse, double *probs, int nthreads)
+{
+    if (wso_check_common(B, L, Hq, Hkv, d) || nb < 0 || !offsets || !out)
+        return -2;
+    for (int b = 0; b < B; ++b) {
+        const int32_t *off = offsets + (int64_t)b * (nb + 1);
+        if (off[0] != 0 || off[nb] != L)
+            return -2;
+        for (int n = 0; n < nb; ++n)
+            if (off[n + 1] < off[n])
+                return -2;
+    }
+    wso_job J;
+    memset(&J, 0, sizeof J);
+    J.kind = WSO_PREFILL;
+    J.B = B; J.Lq = L; J.Hq = Hq; J.Hkv = Hkv; J.d = d;
+    J.scale = scale;
+    J.q = (wso_view){q, dtype, (int64_t)L * Hq * d, (int64_t)Hq * d, d};
+    J.k = (wso_view){k, dtype, (int64_t)L * Hkv * d, (int64_t)Hkv * d, d};
+    J.v = (wso_view){v, dtype, (int64_t)L * Hkv * d, (int64_t)Hkv * d, d};
+    J.offsets = offsets;
+    J.nb = nb;
+    J.rows = rows;
+    J.nrows = nrows;
+    J.out = out;
+    J.lse = lse;
+    J.probs = rows ? probs : NULL;
+    J.lk_max = L;
+    return wso_run(&J, nthreads);
+}
+
+/*
+ * One streaming step: the Lq tokens of a new block attend to the cache
+ * tokens [0, cache_lens[b]) of their stream (all earlier blocks) and to the
+ * whole new block (their own block).  kc, vc: [B][Lc_max][Hkv][d]; q: [B][Lq][Hq][d];
+ * kn, vn: [B][Lq][Hkv][d]; all contiguous.  probs rows have length
+ * Lc_max + Lq (entries past the stream's own key count are left untouched).
+ */
+int wso_step(const void *q, const void *kc, const void *vc,
+             const void *kn, const void *vn, int dtype,
+             int B, int Lq, int Lc_max, const int32_t *cache_lens,
+             int Hq, int Hkv, int d, double scale,
+             const int32_t *rows, int64_t nrows,
+             double *out, double *lse, double *probs, int nthreads)
+{
+    if (wso_check_common(B, Lq, Hq, Hkv, d) || Lc_max < 0 || !cache_lens || !out)
+        return -2;
+    for (int b = 0; b < B; ++b)
+        if (cache_lens[b] < 0 || cache_lens[b] > Lc_max)
+            return -2;
+    wso_job J;
+    memset(&J, 0, sizeof J);
+    J.kind = WSO_STEP;
+    J.B = B; J.Lq = Lq; J.Hq = Hq; J.Hkv = Hkv; J.d = d;
+    J.scale = scale;
+    J.q = (wso_view){q, dtype, (int64_t)Lq * Hq * d, (int64_t)Hq * d, d};
+    J.k = (wso_view){kn, dtype, (int64_t)Lq * Hkv * d, (int64_t)Hkv * d, d};
+    J.v = (wso_view){vn, dtype, (int64_t)Lq * Hkv * d, (int64_t)Hkv * d, d};
+    J.kc = (wso_view){kc, dtype, (int64_t)Lc_max * Hkv * d, (int64_t)Hkv * d, d};
+    J.vc = (wso_view){vc, dtype, (int64_t)Lc_max * Hkv * d, (int64_t)Hkv * d, d};
+    J.cache_lens = cache_lens;
+    J.rows = rows;
+    J.nrows = nrows;
+    J.out = out;
+    J.lse = lse;
+    J.probs = rows ? probs : NULL;
+    J.lk_max = (int64_t)Lc_max + Lq;
+    return wso_run(&J, nthreads);
+}
+
+int wso_mutant(void) { return WSO_MUTANT; }
