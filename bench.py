@@ -1,0 +1,280 @@
+"""Benchmark of block-causal streaming attention on one MI355X.
+
+Headline workload: one streaming step of a 256-token block, MHA 24 x 128,
+against a 4096-token paged cache (64-token pages in seeded random order),
+with the block committed to the cache in the same launch (WS_FUSE_APPEND).
+A "step" is one ws_block_causal_attn_fwd call: plan/validate, append, K/V
+tile fetch, QK^T, online softmax, PV, split combine and epilogue.
+
+Timing: W warm-up steps, then K timed steps bracketed by
+torch.cuda.synchronize(); each step also sits between HIP events recorded on
+the stream the kernels run on (torch's current stream).  The inputs rotate
+over enough device-resident copies (> 512 MB in total) that no copy is still
+in the 256 MB last-level cache when it is used again, so the step reads HBM.
+
+Prints one JSON line (see the metric/roofline/cpu_baseline fields).
+Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-extra]
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import paper_2606_25041_amd as ws  # noqa: E402
+from paper_2606_25041_amd import inputs  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2516.6   # 256 CU x 4096 flop/clk x 2.4 GHz, dense
+ROTATE_BYTES = 600 << 20    # rotation set larger than the 256 MB MALL
+METRIC = "block-causal attn TFLOP/s + per-block step latency (ms) vs KV cache length"
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for p in ws._build.SOURCES:
+        h.update(open(p, "rb").read())
+    return h.hexdigest()[:16]
+
+
+# ---------------------------------------------------------------------------
+# algorithmic work of a workload
+
+def visible_pairs(wl):
+    """Visible (query, key) pairs per (stream, query head)."""
+    if wl.kind == "step":
+        return [int(wl.Lq) * (int(c) + int(wl.Lq)) for c in wl.cache_lens]
+    out = []
+    for off in wl.offsets:
+        lens = np.diff(off.astype(np.int64))
+        out.append(int(np.sum(lens * off[1:].astype(np.int64))))
+    return out
+
+
+def algorithmic_flops(wl):
+    return 4.0 * wl.D * wl.Hq * float(sum(visible_pairs(wl)))
+
+
+def algorithmic_bytes(wl):
+    """Q, K, V and O moved once (K/V once per KV head), plus the appended
+    block's writes when it is committed."""
+    e = 2  # bf16
+    out_e = 4 if wl.out_f32 else 2
+    q = wl.B * wl.Lq * wl.Hq * wl.D * e
+    o = wl.B * wl.Lq * wl.Hq * wl.D * out_e
+    if wl.kind == "step":
+        kv = 2 * sum(int(c) + wl.Lq for c in wl.cache_lens) * wl.Hkv * wl.D * e
+        app = 2 * wl.B * wl.Lq * wl.Hkv * wl.D * e if wl.fuse_append else 0
+        return q + kv + o + app
+    kv = 2 * wl.B * wl.Lq * wl.Hkv * wl.D * e
+    return q + kv + o
+
+
+# ---------------------------------------------------------------------------
+# device setup
+
+class DeviceCase:
+    """Device-resident inputs of one workload (one rotation copy)."""
+
+    def __init__(self, wl, dev):
+        self.wl = wl
+        self.q = wl.q.to(dev)
+        self.out = torch.empty((wl.B, wl.Lq, wl.Hq, wl.D),
+                               dtype=torch.float32 if wl.out_f32 else torch.bfloat16, device=dev)
+        self.lse = torch.empty((wl.B, wl.Hq, wl.Lq), dtype=torch.float32, device=dev)
+        if wl.kind == "step":
+            self.k_new = wl.k_new.contiguous().to(dev)
+            self.v_new = wl.v_new.contiguous().to(dev)
+            self.cache = ws.PagedCache.allocate(wl.num_pages, wl.Hkv, wl.D,
+                                                torch.from_numpy(wl.page_table), device=dev,
+                                                fill_bits=0x7FC1)
+            lens = torch.from_numpy(wl.cache_lens.astype(np.int32))
+            self.lens = (lens, lens.to(dev))
+            kc = wl.k_cache.contiguous().to(dev)
+            vc = wl.v_cache.contiguous().to(dev)
+            n = int(wl.cache_lens.min())
+            assert all(int(c) == n for c in wl.cache_lens)
+            zero = torch.zeros(wl.B, dtype=torch.int32)
+            ws.kv_append(self.cache, (zero, zero.to(dev)), kc[:, :n], vc[:, :n])
+            del kc, vc
+            need = ws.workspace_bytes(ws.WS_OP_STEP, wl.B, wl.Hq, wl.Lq,
+                                      int(wl.cache_lens.max()) + wl.Lq)
+            self.workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+        else:
+            off = torch.from_numpy(wl.offsets.astype(np.int32))
+            self.offsets = (off, off.to(dev))
+            if wl.paged:
+                self.cache = ws.PagedCache.allocate(wl.num_pages, wl.Hkv, wl.D,
+                                                    torch.from_numpy(wl.page_table), device=dev,
+                                                    fill_bits=0x7FC1)
+                zero = torch.zeros(wl.B, dtype=torch.int32)
+                ws.kv_append(self.cache, (zero, zero.to(dev)), wl.k.contiguous().to(dev),
+                             wl.v.contiguous().to(dev))
+                self.k = self.v = None
+            else:
+                self.cache = None
+                self.k = wl.k.to(dev)
+                self.v = wl.v.to(dev)
+
+    def run(self):
+        wl = self.wl
+        if wl.kind == "step":
+            ws.block_causal_attn_fwd(self.q, self.k_new, self.v_new, self.cache, self.lens,
+                                     scale=wl.scale, fuse_append=wl.fuse_append, out=self.out,
+                                     lse=self.lse, want_lse=True, workspace=self.workspace)
+        else:
+            ws.block_causal_prefill(self.q, self.k, self.v, self.offsets, scale=wl.scale,
+                                    cache=self.cache, num_kv_heads=wl.Hkv, out=self.out,
+                                    lse=self.lse, want_lse=True)
+
+
+def time_workload(wl, steps, warmup, dev, rotate=True):
+    """(ms per step from the synchronised wall clock, mean and median of the
+    per-step HIP-event durations in ms)."""
+    nbytes = algorithmic_bytes(wl)
+    copies = max(1, math.ceil(ROTATE_BYTES / nbytes)) if rotate else 1
+    copies = min(copies, 16)
+    log(f"[bench] {wl.name}: building {copies} device copies")
+    cases = [DeviceCase(wl, dev) for _ in range(copies)]
+    torch.cuda.synchronize()
+    for i in range(warmup):
+        cases[i % copies].run()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        ev[i][0].record()
+        cases[i % copies].run()
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3 / steps
+    per = np.array([a.elapsed_time(b) for a, b in ev])
+    log(f"[bench] {wl.name}: wall {wall_ms:.4f} ms/step, events mean {per.mean():.4f} median "
+        f"{np.median(per):.4f} ms")
+    return wall_ms, float(per.mean()), float(np.median(per)), cases[0]
+
+
+def cpu_baseline(wl):
+    """The fp64 oracle (as it stands) on the whole headline step."""
+    import oracle  # test infrastructure: only this baseline leg uses it
+    threads = oracle.default_threads()
+    q, kc, vc = inputs.bf16_bits(wl.q), inputs.bf16_bits(wl.k_cache), inputs.bf16_bits(wl.v_cache)
+    kn, vn = inputs.bf16_bits(wl.k_new), inputs.bf16_bits(wl.v_new)
+    t0 = time.perf_counter()
+    oracle.step(q, kc, vc, wl.cache_lens, kn, vn, wl.scale, nthreads=threads)
+    dt = time.perf_counter() - t0
+    return {"value": algorithmic_flops(wl) / dt / 1e12, "unit": "TFLOP/s", "cores": threads,
+            "kind": "oracle", "seconds": round(dt, 3),
+            "sample": f"the whole headline step ({wl.B * wl.Lq * wl.Hq} query rows x "
+                      f"{int(wl.cache_lens[0]) + wl.Lq} keys), fp64, {threads} threads"}
+
+
+def load_traffic(workload_name):
+    """HBM bytes per launch measured with rocprofv3 counters (FETCH_SIZE,
+    WRITE_SIZE), if a summary for the current kernel source exists."""
+    p = os.path.join(ROOT, "profiles", f"traffic_{workload_name}.json")
+    if not os.path.exists(p):
+        return None
+    d = json.load(open(p))
+    if d.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return d.get("bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-extra", action="store_true", help="headline workload only")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--config", type=int, default=2, help="headline workload index (1-5)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(see the sharding notes in DESIGN.md); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    ws.library()
+
+    wl = inputs.config(args.config)
+    if wl.kind == "step" and args.config == 2:
+        wl.fuse_append = True  # the per-block step commits its block
+    flops, nbytes = algorithmic_flops(wl), algorithmic_bytes(wl)
+    torch.cuda.synchronize()
+    wall_ms, ev_mean, ev_med, _ = time_workload(wl, args.steps, args.warmup, dev)
+    tflops = flops / (wall_ms * 1e-3) / 1e12
+    gbs_kernel = nbytes / (ev_mean * 1e-3) / 1e9
+    ai = flops / nbytes
+    bound = "hbm" if ai < BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9) else "mfma"
+    if bound == "hbm":
+        roof = {"bound": "hbm", "achieved": round(gbs_kernel, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(gbs_kernel / HBM_PEAK_GBS, 4)}
+    else:
+        tf_kernel = flops / (ev_mean * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(tf_kernel, 1), "peak": BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(tf_kernel / BF16_PEAK_TFLOPS, 4)}
+    roof["traffic"] = load_traffic(wl.name)
+    roof["algorithmic_bytes"] = nbytes
+    roof["algorithmic_flops"] = flops
+    roof["kernel_ms"] = round(ev_mean, 5)
+
+    extra = []
+    if not args.no_extra:
+        for idx in (3, 4, 5):
+            if idx == args.config:
+                continue
+            w2 = inputs.config(idx)
+            f2, b2 = algorithmic_flops(w2), algorithmic_bytes(w2)
+            wms, emean, emed, _ = time_workload(w2, max(3, args.steps // 5), 2, dev)
+            extra.append({"workload": w2.name, "ms": round(emean, 4), "TFLOP/s": round(f2 / (emean * 1e-3) / 1e12, 1),
+                          "mfma_frac": round(f2 / (emean * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+                          "GB/s": round(b2 / (emean * 1e-3) / 1e9, 1), "flops": f2, "bytes": b2})
+            del w2
+            torch.cuda.empty_cache()
+
+    cpu = None if args.no_cpu else cpu_baseline(wl)
+    line = {
+        "metric": METRIC,
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall_ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": wl.B, "q_heads": wl.Hq, "kv_heads": wl.Hkv,
+                   "head_dim": wl.D, "block_tokens": wl.Lq,
+                   "cache_tokens": int(wl.cache_lens[0]) if wl.kind == "step" else 0,
+                   "page_size": 64, "fused_append": bool(wl.fuse_append), "seed": wl.seed,
+                   "parallelism": "none (1 GPU)"},
+        "latency_ms_per_block": round(ev_med, 5),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "extra": extra,
+        "gpu": torch.cuda.get_device_name(0),
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

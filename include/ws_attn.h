@@ -1,0 +1,211 @@
+/*
+ * ws_attn.h -- C ABI of the block-causal streaming attention library
+ * (libwsattn.so, gfx950 / MI355X).
+ *
+ * The operation (Wan-Streamer v0.1, Abstract, Sec. 1 with Fig. 1, Sec. 5):
+ * one Transformer runs over an interleaved stream of visual, audio and text
+ * tokens grouped into streaming units ("blocks"); attention is block-causal:
+ * every token sees all tokens of its own block (both directions) and every
+ * token of every earlier block, and nothing later.  Sec. 2.1, Eq. 1 gives the
+ * same conditioning set (unit k conditions on inputs of units <= k and on
+ * responses of units < k).  Sec. 2.4: after the system prefill the
+ * performer keeps a full-history KV cache, appends each received KV slice to
+ * it, and runs the flow-matching solver for the next unit against it; the
+ * current (noisy) unit is not yet part of the cache (Sec. 2.1: clean latents
+ * are appended after denoising).
+ *
+ * For query i with block id beta(i) and keys j with block ids beta(j):
+ *   o_i   = sum_{j : beta(j) <= beta(i)} softmax_j(scale * <q_i, k_j>) v_j
+ *   lse_i = natural log of the softmax denominator (including its max shift)
+ * Grouped-query attention: query head h reads KV head h / (Hq / Hkv).
+ *
+ * Conventions for every entry point
+ * ---------------------------------
+ * - Token tensors are 4-d [batch][tokens][heads][head_dim] described by
+ *   ws_tensor4: the head_dim axis is contiguous; the three other strides are
+ *   in ELEMENTS.  Pointers must be 16-byte aligned and strides multiples of
+ *   8 elements (128-bit loads).
+ * - All device pointers are HIP device memory of the current device; the
+ *   caller owns every buffer (inputs, outputs, cache pool, page tables,
+ *   workspace).  The library allocates no device memory and keeps no state
+ *   between calls except its loaded code object.
+ * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *   All device work is enqueued on it; the call returns after enqueueing
+ *   (stream-ordered, asynchronous).  Host arrays are read only during the
+ *   call.  Calls that write the same memory must be ordered by the caller.
+ * - Every argument is validated on the host before anything is enqueued.
+ *   A non-zero return from validation guarantees that no byte of any
+ *   output, lse, cache pool or workspace was changed.  WS_ERR_HIP reports a
+ *   HIP launch error after validation passed.  Nothing is thrown or aborted
+ *   across the ABI.  ws_last_error() gives a human-readable reason.
+ * - Supported: head_dim 64 or 128; inputs bf16; outputs bf16 or f32;
+ *   page_size 64.
+ * - A call with no token to process (batch == 0, or new_len / seq_len == 0)
+ *   returns WS_OK after checking its scalar arguments, enqueues nothing and
+ *   accepts NULL tensor pointers.
+ */
+#ifndef WS_ATTN_H
+#define WS_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define WS_ABI_VERSION 1
+#define WS_PAGE_SIZE 64
+
+typedef enum {
+    WS_OK = 0,
+    WS_ERR_NULL = 1,        /* a required pointer is NULL                    */
+    WS_ERR_SHAPE = 2,       /* a size is negative or sizes are inconsistent  */
+    WS_ERR_UNSUPPORTED = 3, /* head_dim, dtype or page_size not supported    */
+    WS_ERR_ALIGN = 4,       /* pointer not 16-byte aligned / stride % 8 != 0 */
+    WS_ERR_OFFSETS = 5,     /* block offsets: first != 0, decreasing, last != seq_len */
+    WS_ERR_PAGE = 6,        /* a page id that would be touched is outside [0, num_pages) */
+    WS_ERR_CAPACITY = 7,    /* tokens exceed max_pages_per_seq * page_size   */
+    WS_ERR_HEADS = 8,       /* num_q_heads % num_kv_heads != 0, or head counts differ from the cache's */
+    WS_ERR_WORKSPACE = 9,   /* workspace NULL or smaller than ws_workspace_bytes() */
+    WS_ERR_HIP = 10         /* the HIP runtime reported an error            */
+} ws_status;
+
+enum { WS_DTYPE_BF16 = 1, WS_DTYPE_F32 = 2 };
+
+/* flags of ws_block_causal_attn_fwd */
+enum { WS_FUSE_APPEND = 1 };
+
+/* op codes of ws_workspace_bytes */
+enum { WS_OP_STEP = 1, WS_OP_PREFILL = 2 };
+
+/* A [batch][tokens][heads][head_dim] tensor; head_dim contiguous; strides in elements. */
+typedef struct {
+    void *ptr;
+    int32_t dtype; /* WS_DTYPE_BF16 or WS_DTYPE_F32 */
+    int64_t stride_b, stride_t, stride_h;
+} ws_tensor4;
+
+/*
+ * Paged full-history KV cache (Sec. 2.4: the performer's full-history
+ * cache).  k_pool and v_pool are bf16 [num_pages][num_kv_heads][page_size]
+ * [head_dim], contiguous: one (page, KV head) is page_size * head_dim
+ * consecutive elements.  Logical token position p of stream b lives in
+ * physical page page_table[b][p / page_size], slot p % page_size.
+ * page_table_dev and page_table_host hold the same [batch][max_pages_per_seq]
+ * int32 table (device copy read by kernels, host copy validated by the
+ * library; the caller keeps them equal).  Entries are only read for
+ * positions that a call touches.
+ */
+typedef struct {
+    void *k_pool;
+    void *v_pool;
+    const int32_t *page_table_dev;
+    const int32_t *page_table_host;
+    int32_t num_pages;
+    int32_t page_size;          /* must be WS_PAGE_SIZE */
+    int32_t max_pages_per_seq;
+    int32_t num_kv_heads;
+    int32_t head_dim;
+} ws_paged_kv;
+
+/* WS_ABI_VERSION of the loaded library. */
+int ws_abi_version(void);
+
+/* Static name of a status code ("WS_OK", "WS_ERR_SHAPE", ...). */
+const char *ws_status_string(int status);
+
+/* Reason for the last non-OK status returned on this thread ("" if none). */
+const char *ws_last_error(void);
+
+/*
+ * ws_kv_append -- commit one block of new tokens to the paged cache
+ * (Sec. 2.4: the performer appends the received KV slice to its
+ * full-history cache; Sec. 2.1: clean latents are appended to the history).
+ *
+ * For every stream b < batch and token t < new_len, copies k_new[b][t][h][:]
+ * and v_new[b][t][h][:] (all KV heads h) bit for bit to logical position
+ * cache_lens[b] + t of stream b.  k_new / v_new: bf16 [batch][new_len]
+ * [num_kv_heads][head_dim].  cache_lens_host / cache_lens_dev: int32
+ * [batch], the same values on host (validated) and device.  The cache
+ * lengths are not updated; the caller adds new_len afterwards.
+ * Errors: WS_ERR_NULL, WS_ERR_SHAPE (batch/new_len < 0, cache_lens < 0),
+ * WS_ERR_UNSUPPORTED, WS_ERR_ALIGN, WS_ERR_CAPACITY, WS_ERR_PAGE, WS_ERR_HIP.
+ */
+int ws_kv_append(const ws_paged_kv *kv, int32_t batch,
+                 const int32_t *cache_lens_host, const int32_t *cache_lens_dev,
+                 int32_t new_len, ws_tensor4 k_new, ws_tensor4 v_new, void *stream);
+
+/*
+ * ws_block_causal_attn_fwd -- one streaming step (Sec. 2.4 and Fig. 2: the
+ * performer's solver runs the current unit against the full-history cache;
+ * Sec. 2.1: the current unit is noisy and attends to the clean context).
+ *
+ * The new_len tokens of the new block of stream b see the cache tokens
+ * [0, cache_lens[b]) (all earlier blocks) and all new_len tokens of the new
+ * block itself.  No key is masked except past the end.
+ *   q:           bf16 [batch][new_len][num_q_heads][head_dim]
+ *   k_new/v_new: bf16 [batch][new_len][num_kv_heads][head_dim]; the block's
+ *                own keys and values, read from here (not from the cache)
+ *   kv:          the paged cache; num_kv_heads and head_dim come from it
+ *   cache_lens:  int32 [batch] on host and device, same values
+ *   scale:       multiplies <q, k> (1/sqrt(head_dim) by convention)
+ *   flags:       WS_FUSE_APPEND also commits k_new/v_new at cache_lens in the
+ *                same launch (as ws_kv_append would); the attention result
+ *                is identical.  cache_lens are not updated.
+ *   out:         bf16 or f32 [batch][new_len][num_q_heads][head_dim]
+ *   lse:         NULL or device f32 [batch][num_q_heads][new_len]
+ *   workspace:   device scratch of at least
+ *                ws_workspace_bytes(WS_OP_STEP, batch, num_q_heads, new_len,
+ *                max_b cache_lens[b] + new_len) bytes (NULL allowed when
+ *                that is 0); its contents on entry are ignored.
+ * Errors: WS_ERR_NULL, WS_ERR_SHAPE, WS_ERR_UNSUPPORTED, WS_ERR_ALIGN,
+ * WS_ERR_HEADS, WS_ERR_CAPACITY, WS_ERR_PAGE, WS_ERR_WORKSPACE, WS_ERR_HIP.
+ */
+int ws_block_causal_attn_fwd(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new,
+                             const ws_paged_kv *kv,
+                             const int32_t *cache_lens_host, const int32_t *cache_lens_dev,
+                             int32_t batch, int32_t new_len, int32_t num_q_heads,
+                             float scale, int32_t flags,
+                             ws_tensor4 out, float *lse,
+                             void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * ws_block_causal_prefill -- block-causal attention over whole sequences
+ * (Sec. 2.4: the system prefill that builds the initial full-history state;
+ * Sec. 2.3: training uses the same causal format as inference).
+ *
+ * Every stream holds seq_len tokens split into num_blocks consecutive blocks
+ * with boundaries block_offsets[b][0..num_blocks] (first 0, non-decreasing,
+ * last seq_len; zero-length blocks are allowed and own no token).  Token i
+ * sees every token j < end of i's block.
+ *   q:    bf16 [batch][seq_len][num_q_heads][head_dim]
+ *   k, v: bf16 [batch][seq_len][num_kv_heads][head_dim], or k.ptr == v.ptr ==
+ *         NULL to read keys and values from kv_or_null (positions
+ *         [0, seq_len) of each stream, e.g. filled by ws_kv_append)
+ *   block_offsets_host / _dev: int32 [batch][num_blocks + 1], same values
+ *   out:  bf16 or f32 [batch][seq_len][num_q_heads][head_dim]
+ *   lse:  NULL or device f32 [batch][num_q_heads][seq_len]
+ * Errors: WS_ERR_NULL, WS_ERR_SHAPE, WS_ERR_UNSUPPORTED, WS_ERR_ALIGN,
+ * WS_ERR_HEADS, WS_ERR_OFFSETS, WS_ERR_CAPACITY, WS_ERR_PAGE, WS_ERR_HIP.
+ */
+int ws_block_causal_prefill(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v,
+                            const ws_paged_kv *kv_or_null,
+                            const int32_t *block_offsets_host, const int32_t *block_offsets_dev,
+                            int32_t batch, int32_t seq_len, int32_t num_blocks,
+                            int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                            float scale, ws_tensor4 out, float *lse, void *stream);
+
+/*
+ * Workspace bytes ws_block_causal_attn_fwd needs for this shape (op =
+ * WS_OP_STEP; max_k = largest cache_lens[b] + new_len).  WS_OP_PREFILL
+ * returns 0.  Pure host arithmetic; returns 0 for invalid arguments.
+ */
+size_t ws_workspace_bytes(int32_t op, int32_t batch, int32_t num_q_heads,
+                          int32_t max_q, int32_t max_k);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WS_ATTN_H */

@@ -1,0 +1,335 @@
+// C ABI of libwsattn: host-side validation and launch planning.
+//
+// Plain C++ (no HIP headers): every argument is checked here before any
+// device work is enqueued, so a rejected call leaves all device memory
+// untouched.  Kernels are reached through the launchers of ws_kernels.hip.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+
+#include "../../include/ws_attn.h"
+#include "ws_kernels.h"
+
+namespace {
+
+thread_local char g_err[512];
+
+int fail(int status, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+int ok() {
+    g_err[0] = '\0';
+    return WS_OK;
+}
+
+constexpr int TARGET_WORKGROUPS = 256;  // one wave of work-groups on 256 CUs
+constexpr int WS_MAX_SPLITS = 32;
+constexpr int WS_MAX_HEAD_DIM = 128;
+
+int env_int(const char *name, int dflt) {
+    const char *s = std::getenv(name);
+    if (!s || !*s) return dflt;
+    return std::atoi(s);
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Checks pointer, dtype, alignment and strides of one token tensor.
+int check_tensor(const char *name, const ws_tensor4 &t, bool allow_f32) {
+    if (!t.ptr) return fail(WS_ERR_NULL, "%s.ptr is NULL", name);
+    if (t.dtype != WS_DTYPE_BF16 && !(allow_f32 && t.dtype == WS_DTYPE_F32))
+        return fail(WS_ERR_UNSUPPORTED, "%s.dtype %d not supported", name, (int)t.dtype);
+    if (t.stride_b < 0 || t.stride_t < 0 || t.stride_h < 0)
+        return fail(WS_ERR_SHAPE, "%s has a negative stride", name);
+    const int64_t q = (t.dtype == WS_DTYPE_BF16) ? 8 : 4;  // elements per 16 bytes
+    if (!aligned16(t.ptr) || t.stride_b % q || t.stride_t % q || t.stride_h % q)
+        return fail(WS_ERR_ALIGN, "%s: pointer must be 16-byte aligned and strides multiples of 16 bytes", name);
+    return WS_OK;
+}
+
+int check_head_dim(int d) {
+    if (d != 64 && d != 128) return fail(WS_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", d);
+    return WS_OK;
+}
+
+int check_paged(const ws_paged_kv *kv) {
+    if (!kv) return fail(WS_ERR_NULL, "kv is NULL");
+    if (!kv->k_pool || !kv->v_pool) return fail(WS_ERR_NULL, "kv pool pointer is NULL");
+    if (!kv->page_table_dev || !kv->page_table_host) return fail(WS_ERR_NULL, "kv page table pointer is NULL");
+    if (kv->num_pages <= 0 || kv->max_pages_per_seq < 0 || kv->num_kv_heads <= 0)
+        return fail(WS_ERR_SHAPE, "kv: num_pages %d, max_pages_per_seq %d, num_kv_heads %d",
+                    (int)kv->num_pages, (int)kv->max_pages_per_seq, (int)kv->num_kv_heads);
+    if (kv->page_size != WS_PAGE_SIZE)
+        return fail(WS_ERR_UNSUPPORTED, "page_size %d not supported (only %d)", (int)kv->page_size, WS_PAGE_SIZE);
+    if (int rc = check_head_dim(kv->head_dim)) return rc;
+    if (!aligned16(kv->k_pool) || !aligned16(kv->v_pool))
+        return fail(WS_ERR_ALIGN, "kv pools must be 16-byte aligned");
+    return WS_OK;
+}
+
+// Every page that positions [0, n) of stream b live in must exist.
+int check_pages(const ws_paged_kv *kv, int b, int64_t n) {
+    if (n > (int64_t)kv->max_pages_per_seq * kv->page_size)
+        return fail(WS_ERR_CAPACITY, "stream %d needs %lld tokens but holds at most %lld", b,
+                    (long long)n, (long long)kv->max_pages_per_seq * kv->page_size);
+    const int64_t pages = (n + kv->page_size - 1) / kv->page_size;
+    const int32_t *row = kv->page_table_host + (int64_t)b * kv->max_pages_per_seq;
+    for (int64_t p = 0; p < pages; ++p)
+        if (row[p] < 0 || row[p] >= kv->num_pages)
+            return fail(WS_ERR_PAGE, "page_table[%d][%lld] = %d outside [0, %d)", b, (long long)p,
+                        (int)row[p], (int)kv->num_pages);
+    return WS_OK;
+}
+
+struct StepPlan {
+    ws::TileShape shape;
+    int nqt;
+    int nsplit;
+};
+
+// Query tile and KV split count of a streaming step.  Splits are added only
+// until about one work-group per CU exists, and every split keeps at least
+// two 64-key tiles.
+StepPlan plan_step(int batch, int hq, int lq, int64_t max_k) {
+    StepPlan p;
+    const int qt_env = env_int("WS_QTILE", 0);
+    if (qt_env == 128) p.shape = {1, 4};
+    else if (qt_env == 256) p.shape = {2, 4};
+    else p.shape = (lq >= 256) ? ws::TileShape{2, 4} : ws::TileShape{1, 4};
+    const int qt = p.shape.qtile();
+    p.nqt = (lq + qt - 1) / qt;
+    const int64_t base = (int64_t)batch * hq * p.nqt;
+    const int64_t ntiles = (max_k + 63) / 64;
+    int64_t ns = 1;
+    if (base > 0 && base < TARGET_WORKGROUPS) ns = (TARGET_WORKGROUPS + base - 1) / base;
+    if (ns > ntiles / 2) ns = ntiles / 2;
+    if (ns > WS_MAX_SPLITS) ns = WS_MAX_SPLITS;
+    if (ns < 1) ns = 1;
+    const int s_env = env_int("WS_SPLITS", 0);
+    if (s_env > 0) ns = s_env > WS_MAX_SPLITS ? WS_MAX_SPLITS : s_env;
+    p.nsplit = (int)ns;
+    return p;
+}
+
+size_t step_workspace(const StepPlan &p, int batch, int hq, int lq) {
+    if (p.nsplit <= 1) return 0;
+    return (size_t)p.nsplit * batch * hq * lq * (WS_MAX_HEAD_DIM + 2) * sizeof(float);
+}
+
+ws::TileShape plan_prefill(int seq_len) {
+    const int qt_env = env_int("WS_QTILE", 0);
+    if (qt_env == 128) return {1, 4};
+    if (qt_env == 256) return {2, 4};
+    return seq_len >= 512 ? ws::TileShape{2, 4} : ws::TileShape{1, 4};
+}
+
+// Total work items; fails when the grid would not fit the kernel's int math.
+bool finish_work(ws::AttnArgs &a) {
+    const int64_t n = (int64_t)a.B * a.Hq * a.nqt * a.nsplit;
+    if (n > (int64_t)1 << 30) return false;
+    a.n_work = (int32_t)n;
+    a.per_xcd = (a.n_work + 7) / 8;
+    return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ws_abi_version(void) { return WS_ABI_VERSION; }
+
+const char *ws_status_string(int status) {
+    switch (status) {
+        case WS_OK: return "WS_OK";
+        case WS_ERR_NULL: return "WS_ERR_NULL";
+        case WS_ERR_SHAPE: return "WS_ERR_SHAPE";
+        case WS_ERR_UNSUPPORTED: return "WS_ERR_UNSUPPORTED";
+        case WS_ERR_ALIGN: return "WS_ERR_ALIGN";
+        case WS_ERR_OFFSETS: return "WS_ERR_OFFSETS";
+        case WS_ERR_PAGE: return "WS_ERR_PAGE";
+        case WS_ERR_CAPACITY: return "WS_ERR_CAPACITY";
+        case WS_ERR_HEADS: return "WS_ERR_HEADS";
+        case WS_ERR_WORKSPACE: return "WS_ERR_WORKSPACE";
+        case WS_ERR_HIP: return "WS_ERR_HIP";
+        default: return "WS_ERR_UNKNOWN";
+    }
+}
+
+const char *ws_last_error(void) { return g_err; }
+
+size_t ws_workspace_bytes(int32_t op, int32_t batch, int32_t num_q_heads, int32_t max_q, int32_t max_k) {
+    if (op != WS_OP_STEP) return 0;
+    if (batch <= 0 || num_q_heads <= 0 || max_q <= 0 || max_k < max_q) return 0;
+    const StepPlan p = plan_step(batch, num_q_heads, max_q, max_k);
+    return step_workspace(p, batch, num_q_heads, max_q);
+}
+
+int ws_kv_append(const ws_paged_kv *kv, int32_t batch, const int32_t *cache_lens_host,
+                 const int32_t *cache_lens_dev, int32_t new_len, ws_tensor4 k_new, ws_tensor4 v_new,
+                 void *stream) {
+    if (int rc = check_paged(kv)) return rc;
+    if (!cache_lens_host || !cache_lens_dev) return fail(WS_ERR_NULL, "cache_lens pointer is NULL");
+    if (batch < 0 || new_len < 0) return fail(WS_ERR_SHAPE, "batch %d, new_len %d", (int)batch, (int)new_len);
+    if (batch == 0 || new_len == 0) return ok();  // nothing is read or written
+    if (int rc = check_tensor("k_new", k_new, false)) return rc;
+    if (int rc = check_tensor("v_new", v_new, false)) return rc;
+    for (int b = 0; b < batch; ++b) {
+        if (cache_lens_host[b] < 0) return fail(WS_ERR_SHAPE, "cache_lens[%d] = %d", b, (int)cache_lens_host[b]);
+        if (int rc = check_pages(kv, b, (int64_t)cache_lens_host[b] + new_len)) return rc;
+    }
+    ws::AppendArgs a{};
+    a.kn = (const uint16_t *)k_new.ptr;
+    a.vn = (const uint16_t *)v_new.ptr;
+    a.kn_sb = k_new.stride_b; a.kn_st = k_new.stride_t; a.kn_sh = k_new.stride_h;
+    a.vn_sb = v_new.stride_b; a.vn_st = v_new.stride_t; a.vn_sh = v_new.stride_h;
+    a.kpool = (uint16_t *)kv->k_pool;
+    a.vpool = (uint16_t *)kv->v_pool;
+    a.page_table = kv->page_table_dev;
+    a.max_pages = kv->max_pages_per_seq;
+    a.cache_lens = cache_lens_dev;
+    a.B = batch; a.Ln = new_len; a.Hkv = kv->num_kv_heads; a.D = kv->head_dim;
+    if (int e = ws::launch_append(a, stream)) return fail(WS_ERR_HIP, "append launch failed (hip error %d)", e);
+    return ok();
+}
+
+int ws_block_causal_attn_fwd(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_kv *kv,
+                             const int32_t *cache_lens_host, const int32_t *cache_lens_dev, int32_t batch,
+                             int32_t new_len, int32_t num_q_heads, float scale, int32_t flags,
+                             ws_tensor4 out, float *lse, void *workspace, size_t workspace_bytes,
+                             void *stream) {
+    if (int rc = check_paged(kv)) return rc;
+    if (!cache_lens_host || !cache_lens_dev) return fail(WS_ERR_NULL, "cache_lens pointer is NULL");
+    if (batch < 0 || new_len < 0 || num_q_heads <= 0)
+        return fail(WS_ERR_SHAPE, "batch %d, new_len %d, num_q_heads %d", (int)batch, (int)new_len, (int)num_q_heads);
+    if (batch == 0 || new_len == 0) return ok();  // no query row: nothing is read or written
+    if (int rc = check_tensor("q", q, false)) return rc;
+    if (int rc = check_tensor("k_new", k_new, false)) return rc;
+    if (int rc = check_tensor("v_new", v_new, false)) return rc;
+    if (int rc = check_tensor("out", out, true)) return rc;
+    if (flags & ~WS_FUSE_APPEND) return fail(WS_ERR_UNSUPPORTED, "unknown flags 0x%x", (unsigned)flags);
+    if (!(scale > 0.f) || !std::isfinite(scale)) return fail(WS_ERR_UNSUPPORTED, "scale must be finite and > 0");
+    if (num_q_heads % kv->num_kv_heads)
+        return fail(WS_ERR_HEADS, "num_q_heads %d not a multiple of num_kv_heads %d", (int)num_q_heads,
+                    (int)kv->num_kv_heads);
+    if (lse && ((uintptr_t)lse & 3u)) return fail(WS_ERR_ALIGN, "lse must be 4-byte aligned");
+    const bool fuse = (flags & WS_FUSE_APPEND) != 0;
+    int64_t max_k = 0;
+    for (int b = 0; b < batch; ++b) {
+        if (cache_lens_host[b] < 0) return fail(WS_ERR_SHAPE, "cache_lens[%d] = %d", b, (int)cache_lens_host[b]);
+        const int64_t need = (int64_t)cache_lens_host[b] + (fuse ? new_len : 0);
+        if (int rc = check_pages(kv, b, need)) return rc;
+        if ((int64_t)cache_lens_host[b] + new_len > max_k) max_k = (int64_t)cache_lens_host[b] + new_len;
+    }
+    if (max_k > INT32_MAX) return fail(WS_ERR_SHAPE, "too many keys");
+    const StepPlan plan = plan_step(batch, num_q_heads, new_len, max_k);
+    const size_t need_ws = step_workspace(plan, batch, num_q_heads, new_len);
+    if (need_ws > 0 && (!workspace || workspace_bytes < need_ws || !aligned16(workspace)))
+        return fail(WS_ERR_WORKSPACE, "workspace needs %zu bytes (16-byte aligned), got %zu", need_ws,
+                    workspace ? workspace_bytes : (size_t)0);
+
+    ws::AttnArgs a{};
+    a.q = (const uint16_t *)q.ptr; a.q_sb = q.stride_b; a.q_st = q.stride_t; a.q_sh = q.stride_h;
+    a.kc = (const uint16_t *)k_new.ptr; a.kc_sb = k_new.stride_b; a.kc_st = k_new.stride_t; a.kc_sh = k_new.stride_h;
+    a.vc = (const uint16_t *)v_new.ptr; a.vc_sb = v_new.stride_b; a.vc_st = v_new.stride_t; a.vc_sh = v_new.stride_h;
+    a.kpool = (uint16_t *)kv->k_pool; a.vpool = (uint16_t *)kv->v_pool;
+    a.page_table = kv->page_table_dev; a.max_pages = kv->max_pages_per_seq;
+    a.cache_lens = cache_lens_dev;
+    a.out = out.ptr; a.o_sb = out.stride_b; a.o_st = out.stride_t; a.o_sh = out.stride_h;
+    a.out_f32 = out.dtype == WS_DTYPE_F32;
+    a.lse = lse;
+    a.B = batch; a.Lq = new_len; a.Hq = num_q_heads; a.Hkv = kv->num_kv_heads; a.G = num_q_heads / kv->num_kv_heads;
+    a.mode = ws::MODE_STEP;
+    a.fuse_append = fuse;
+    a.nsplit = plan.nsplit;
+    a.nqt = plan.nqt;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    if (plan.nsplit > 1) {
+        a.part_o = (float *)workspace;
+        a.part_ml = a.part_o + (size_t)plan.nsplit * batch * num_q_heads * new_len * kv->head_dim;
+    }
+    if (!finish_work(a)) return fail(WS_ERR_SHAPE, "too many work items");
+    if (int e = ws::launch_attention(a, kv->head_dim, plan.shape, stream))
+        return fail(WS_ERR_HIP, "attention launch failed (hip error %d)", e);
+    if (plan.nsplit > 1)
+        if (int e = ws::launch_combine(a, kv->head_dim, stream))
+            return fail(WS_ERR_HIP, "combine launch failed (hip error %d)", e);
+    return ok();
+}
+
+int ws_block_causal_prefill(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, const ws_paged_kv *kv_or_null,
+                            const int32_t *block_offsets_host, const int32_t *block_offsets_dev,
+                            int32_t batch, int32_t seq_len, int32_t num_blocks, int32_t num_q_heads,
+                            int32_t num_kv_heads, int32_t head_dim, float scale, ws_tensor4 out,
+                            float *lse, void *stream) {
+    if (batch < 0 || seq_len < 0 || num_blocks < 0 || num_q_heads <= 0 || num_kv_heads <= 0)
+        return fail(WS_ERR_SHAPE, "batch %d, seq_len %d, num_blocks %d, heads %d/%d", (int)batch, (int)seq_len,
+                    (int)num_blocks, (int)num_q_heads, (int)num_kv_heads);
+    if (batch == 0 || seq_len == 0) return ok();  // no token: nothing is read or written
+    const bool paged = !k.ptr && !v.ptr;
+    if (paged) {
+        if (!kv_or_null) return fail(WS_ERR_NULL, "k/v are NULL and no paged cache was given");
+        if (int rc = check_paged(kv_or_null)) return rc;
+    } else {
+        if (int rc = check_tensor("k", k, false)) return rc;
+        if (int rc = check_tensor("v", v, false)) return rc;
+    }
+    if (int rc = check_tensor("q", q, false)) return rc;
+    if (int rc = check_tensor("out", out, true)) return rc;
+    if (!block_offsets_host || !block_offsets_dev) return fail(WS_ERR_NULL, "block offsets pointer is NULL");
+    if (int rc = check_head_dim(head_dim)) return rc;
+    if (!(scale > 0.f) || !std::isfinite(scale)) return fail(WS_ERR_UNSUPPORTED, "scale must be finite and > 0");
+    if (num_q_heads % num_kv_heads)
+        return fail(WS_ERR_HEADS, "num_q_heads %d not a multiple of num_kv_heads %d", (int)num_q_heads,
+                    (int)num_kv_heads);
+    if (paged && (kv_or_null->num_kv_heads != num_kv_heads || kv_or_null->head_dim != head_dim))
+        return fail(WS_ERR_HEADS, "paged cache has %d KV heads of dim %d, call says %d of dim %d",
+                    (int)kv_or_null->num_kv_heads, (int)kv_or_null->head_dim, (int)num_kv_heads, (int)head_dim);
+    if (lse && ((uintptr_t)lse & 3u)) return fail(WS_ERR_ALIGN, "lse must be 4-byte aligned");
+    for (int b = 0; b < batch; ++b) {
+        const int32_t *off = block_offsets_host + (int64_t)b * (num_blocks + 1);
+        if (off[0] != 0) return fail(WS_ERR_OFFSETS, "block_offsets[%d][0] = %d, must be 0", b, (int)off[0]);
+        for (int n = 0; n < num_blocks; ++n)
+            if (off[n + 1] < off[n])
+                return fail(WS_ERR_OFFSETS, "block_offsets[%d] decreases at %d", b, n + 1);
+        if (off[num_blocks] != seq_len)
+            return fail(WS_ERR_OFFSETS, "block_offsets[%d][%d] = %d, must equal seq_len %d", b, (int)num_blocks,
+                        (int)off[num_blocks], (int)seq_len);
+        if (paged)
+            if (int rc = check_pages(kv_or_null, b, seq_len)) return rc;
+    }
+
+    const ws::TileShape shape = plan_prefill(seq_len);
+    ws::AttnArgs a{};
+    a.q = (const uint16_t *)q.ptr; a.q_sb = q.stride_b; a.q_st = q.stride_t; a.q_sh = q.stride_h;
+    if (paged) {
+        a.kpool = (uint16_t *)kv_or_null->k_pool; a.vpool = (uint16_t *)kv_or_null->v_pool;
+        a.page_table = kv_or_null->page_table_dev; a.max_pages = kv_or_null->max_pages_per_seq;
+        a.paged = 1;
+    } else {
+        a.kc = (const uint16_t *)k.ptr; a.kc_sb = k.stride_b; a.kc_st = k.stride_t; a.kc_sh = k.stride_h;
+        a.vc = (const uint16_t *)v.ptr; a.vc_sb = v.stride_b; a.vc_st = v.stride_t; a.vc_sh = v.stride_h;
+    }
+    a.offsets = block_offsets_dev;
+    a.nb = num_blocks;
+    a.out = out.ptr; a.o_sb = out.stride_b; a.o_st = out.stride_t; a.o_sh = out.stride_h;
+    a.out_f32 = out.dtype == WS_DTYPE_F32;
+    a.lse = lse;
+    a.B = batch; a.Lq = seq_len; a.Hq = num_q_heads; a.Hkv = num_kv_heads; a.G = num_q_heads / num_kv_heads;
+    a.mode = ws::MODE_PREFILL;
+    a.nsplit = 1;
+    a.nqt = (seq_len + shape.qtile() - 1) / shape.qtile();
+    a.scale_log2 = scale * 1.4426950408889634f;
+    if (!finish_work(a)) return fail(WS_ERR_SHAPE, "too many work items");
+    if (int e = ws::launch_attention(a, head_dim, shape, stream))
+        return fail(WS_ERR_HIP, "prefill launch failed (hip error %d)", e);
+    return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,70 @@
+// Internal interface between the host-side validation/planning code
+// (ws_api.cpp, no HIP headers) and the gfx950 kernels (ws_kernels.hip).
+#pragma once
+
+#include <stdint.h>
+
+namespace ws {
+
+enum { MODE_PREFILL = 0, MODE_STEP = 1 };
+
+// Everything one attention launch needs.  Element strides; bf16 data is
+// carried as uint16_t bit patterns.
+struct AttnArgs {
+    // queries [B][Lq][Hq][D]
+    const uint16_t *q;
+    int64_t q_sb, q_st, q_sh;
+    // contiguous keys/values: the prefill's K/V, or the step's own new block
+    const uint16_t *kc, *vc;
+    int64_t kc_sb, kc_st, kc_sh;
+    int64_t vc_sb, vc_st, vc_sh;
+    // paged pool [pages][Hkv][64][D] and its table [B][max_pages]
+    uint16_t *kpool, *vpool;
+    const int32_t *page_table;
+    int32_t max_pages;
+    // step: cache length of each stream [B]; prefill: block offsets [B][nb+1]
+    const int32_t *cache_lens;
+    const int32_t *offsets;
+    int32_t nb;
+    // output [B][Lq][Hq][D] (bf16 or f32) and lse [B][Hq][Lq] (nullable)
+    void *out;
+    int64_t o_sb, o_st, o_sh;
+    int32_t out_f32;
+    float *lse;
+    // split-KV partials: o [S][B][Hq][Lq][D] f32, (m, l) [S][B][Hq][Lq][2]
+    float *part_o, *part_ml;
+    int32_t B, Lq, Hq, Hkv, G;
+    int32_t mode;        // MODE_PREFILL or MODE_STEP
+    int32_t paged;       // prefill only: keys/values come from the pool
+    int32_t fuse_append; // step only: also commit kc/vc to the pool
+    int32_t nsplit;      // KV splits per (b, hq, q-tile)
+    int32_t nqt;         // q-tiles per (b, hq)
+    int32_t n_work;      // B * Hq * nqt * nsplit
+    int32_t per_xcd;     // ceil(n_work / 8)
+    float scale_log2;    // scale * log2(e)
+};
+
+struct AppendArgs {
+    const uint16_t *kn, *vn;
+    int64_t kn_sb, kn_st, kn_sh;
+    int64_t vn_sb, vn_st, vn_sh;
+    uint16_t *kpool, *vpool;
+    const int32_t *page_table;
+    int32_t max_pages;
+    const int32_t *cache_lens;
+    int32_t B, Ln, Hkv, D;
+};
+
+// Launch shapes compiled into the library.
+struct TileShape {
+    int nb;  // 32-query column blocks per wave
+    int nw;  // waves per work-group
+    int qtile() const { return nb * nw * 32; }
+};
+
+// Each returns 0 or a HIP error code (hipError_t as int).
+int launch_attention(const AttnArgs &a, int head_dim, TileShape shape, void *stream);
+int launch_combine(const AttnArgs &a, int head_dim, void *stream);
+int launch_append(const AppendArgs &a, void *stream);
+
+}  // namespace ws

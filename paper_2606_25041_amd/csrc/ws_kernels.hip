@@ -1,0 +1,484 @@
+// gfx950 (MI355X) kernels for block-causal streaming attention.
+//
+// Block-causal rule (Wan-Streamer v0.1, Abstract; Sec. 1 with Fig. 1): a
+// token sees its whole own block and every earlier block.  The step kernel
+// runs the performer's current unit against its full-history cache
+// (Sec. 2.4); the prefill kernel covers whole sequences (Sec. 2.4, system
+// prefill); the append kernel commits a KV slice to the paged cache
+// (Sec. 2.4).
+//
+// Attention kernel design (one work-group = one (stream, query head,
+// query tile, KV split) work item; waves own 32*NB query rows each):
+//  * S^T = K Q^T on v_mfma_f32_32x32x16_bf16: K (A operand) from LDS, Q (B
+//    operand) resident in registers.  In the 32x32 accumulator layout a lane
+//    owns one query column and 16 keys, so row max/sum are in-lane plus one
+//    v_permlane32_swap per 64-key tile.
+//  * Online softmax in the log2 domain (scale*log2(e) folded into one FMA),
+//    fp32 running max/sum per lane.
+//  * O^T += V^T P^T on the same MFMA: P stays in registers (the accumulator
+//    layout of S^T is exactly the B-operand layout once the 16 keys of each
+//    MFMA step are permuted consistently on both operands); V is read with
+//    ds_read_b64_tr_b16 from a row-major LDS tile, so no transpose pass.
+//    Each lane owns one query column of O^T, so the softmax rescale is a
+//    per-lane scalar multiply.
+//  * K/V tiles of 64 keys (= one cache page) are staged global -> VGPR ->
+//    LDS with 128-bit loads, double-buffered in LDS (one barrier per tile),
+//    the next tile's loads in flight during the current tile's MFMAs.
+//  * Tiles past the last visible key of the query tile are never loaded
+//    (block-granularity skip); tiles fully visible to every row of the query
+//    tile run without element masks; only the tiles straddling a block
+//    boundary (or the end of the keys) apply per-element masks.
+//  * Work items are ordered by KV group (stream, KV head) and mapped
+//    XCD-aware: consecutive logical items land on the same XCD so query heads
+//    and query tiles that read the same K/V share that XCD's L2.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "ws_kernels.h"
+
+namespace ws {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int KT = 64;        // keys per tile (= page size)
+constexpr int NUM_XCD = 8;    // MI355X: 8 XCDs, work-groups dispatched round-robin
+
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// max / sum of a value over lanes l and l^32 (same query column, other keys)
+__device__ __forceinline__ float halves_max(float x) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float halves_sum(float x) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// End (exclusive) of the block that holds token i: the first offset > i.
+__device__ __forceinline__ int block_end(const int32_t *off, int nb, int i) {
+    int lo = 1, hi = nb;  // answer index in [1, nb]
+    while (lo < hi) {
+        int mid = (lo + hi) >> 1;
+        if (off[mid] > i) hi = mid; else lo = mid + 1;
+    }
+    return off[lo];
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    __bf16 a = (__bf16)lo, b = (__bf16)hi;
+    return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+
+template <int D, int NB, int NW>
+__global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
+    constexpr int NT = NW * 64;
+    constexpr int QT = NW * 32 * NB;
+    constexpr int CH = D / 8;             // 16-byte chunks per key row
+    constexpr int KP = D * 2 + 16;        // K row pitch in LDS (bytes): conflict-free b128 reads
+    constexpr int VP = D * 2 + 32;        // V row pitch in LDS (bytes): conflict-free transpose reads
+    constexpr int KBYTES = KT * KP;
+    constexpr int VBYTES = KT * VP;
+    constexpr int LOADS = KT * CH / NT;   // 16-byte chunks per thread per tile, each of K and V
+    constexpr int KK = D / 16;            // MFMA k-steps over head_dim for S
+    constexpr int MD = D / 32;            // 32-row blocks of head_dim for O^T
+    static_assert((KT * CH) % NT == 0, "tile chunks must divide among threads");
+    __shared__ __attribute__((aligned(16))) char smem[2 * (KBYTES + VBYTES)];
+
+    // ---- work item ------------------------------------------------------
+    const int bid = blockIdx.x;
+    const int w = (bid % NUM_XCD) * a.per_xcd + bid / NUM_XCD;
+    if (w >= a.n_work) return;
+    const int per_group = a.G * a.nqt * a.nsplit;
+    const int group = w / per_group;
+    const int idx = w - group * per_group;
+    const int qi = idx / (a.G * a.nsplit);
+    const int rem = idx - qi * (a.G * a.nsplit);
+    const int split = rem / a.G;
+    const int hh = rem - split * a.G;
+    const int b = group / a.Hkv;
+    const int kvh = group - b * a.Hkv;
+    const int hq = kvh * a.G + hh;
+    const bool step = a.mode == MODE_STEP;
+    const int qt = step ? qi : (a.nqt - 1 - qi);  // prefill: heaviest tiles first
+    const int q0 = qt * QT;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int hf = lane >> 5;     // which half of the wave
+    const int l32 = lane & 31;
+
+    // ---- key range ------------------------------------------------------
+    const int32_t *offs = step ? nullptr : a.offsets + (int64_t)b * (a.nb + 1);
+    int n_pool, k_hi, kfull;
+    if (step) {
+        n_pool = a.cache_lens[b];
+        k_hi = n_pool + a.Lq;
+        kfull = k_hi;
+    } else {
+        n_pool = a.paged ? a.Lq : 0;
+        const int q_last = min(q0 + QT, a.Lq) - 1;
+        k_hi = block_end(offs, a.nb, q_last);
+        kfull = block_end(offs, a.nb, q0);
+    }
+    const int ntile = (k_hi + KT - 1) / KT;
+    const int t_begin = (int)((int64_t)split * ntile / a.nsplit);
+    const int t_end = (int)((int64_t)(split + 1) * ntile / a.nsplit);
+
+    // ---- fused append: this work item's share of the new block -------------
+    // The G query heads of a group share one KV head, so only the items of
+    // its first head write; they split the new tokens evenly among them.
+    if (step && a.fuse_append && hh == 0) {
+        const int napp = a.nqt * a.nsplit;
+        const int ai = qi * a.nsplit + split;
+        const int s0 = (int)((int64_t)ai * a.Lq / napp);
+        const int s1 = (int)((int64_t)(ai + 1) * a.Lq / napp);
+        for (int u = tid; u < (s1 - s0) * CH; u += NT) {
+            const int t = s0 + u / CH, c = u % CH;
+            const int pos = n_pool + t;
+            const int page = a.page_table[(int64_t)b * a.max_pages + (pos >> 6)];
+            const int64_t dst = (((int64_t)page * a.Hkv + kvh) * KT + (pos & 63)) * D + 8 * c;
+            *(u32x4 *)(a.kpool + dst) = *(const u32x4 *)(a.kc + b * a.kc_sb + (int64_t)t * a.kc_st + kvh * a.kc_sh + 8 * c);
+            *(u32x4 *)(a.vpool + dst) = *(const u32x4 *)(a.vc + b * a.vc_sb + (int64_t)t * a.vc_st + kvh * a.vc_sh + 8 * c);
+        }
+    }
+
+    // ---- this lane's query rows -----------------------------------------
+    int rows[NB], kend[NB];
+    bf16x8 qf[NB][KK];
+#pragma unroll
+    for (int n = 0; n < NB; ++n) {
+        rows[n] = q0 + wave * 32 * NB + n * 32 + l32;
+        const int rc = min(rows[n], a.Lq - 1);
+        kend[n] = step ? k_hi : block_end(offs, a.nb, rc);
+        const uint16_t *qp = a.q + b * a.q_sb + (int64_t)rc * a.q_st + hq * a.q_sh + 8 * hf;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) qf[n][kk] = *(const bf16x8 *)(qp + 16 * kk);
+    }
+
+    f32x16 o[NB][MD];
+    float m[NB], l[NB];
+#pragma unroll
+    for (int n = 0; n < NB; ++n) {
+        m[n] = -INFINITY;
+        l[n] = 0.f;
+#pragma unroll
+        for (int md = 0; md < MD; ++md)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) o[n][md][v] = 0.f;
+    }
+
+    // ---- tile staging ---------------------------------------------------
+    u32x4 kreg[LOADS], vreg[LOADS];
+    auto load_tile = [&](int kt) {
+        int page = 0;
+        if (kt < n_pool) page = a.page_table[(int64_t)b * a.max_pages + (kt >> 6)];
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) {
+            const int u = tid + i * NT;
+            const int row = u / CH, c = u % CH;
+            const int j = min(kt + row, k_hi - 1);  // past the end: repeat a valid row (masked)
+            if (j < n_pool) {
+                const int64_t off = (((int64_t)page * a.Hkv + kvh) * KT + (j & 63)) * D + 8 * c;
+                kreg[i] = *(const u32x4 *)(a.kpool + off);
+                vreg[i] = *(const u32x4 *)(a.vpool + off);
+            } else {
+                const int jj = j - n_pool;
+                kreg[i] = *(const u32x4 *)(a.kc + b * a.kc_sb + (int64_t)jj * a.kc_st + kvh * a.kc_sh + 8 * c);
+                vreg[i] = *(const u32x4 *)(a.vc + b * a.vc_sb + (int64_t)jj * a.vc_st + kvh * a.vc_sh + 8 * c);
+            }
+        }
+    };
+    auto store_tile = [&](int buf) {
+        char *ks = smem + buf * (KBYTES + VBYTES);
+        char *vs = ks + KBYTES;
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) {
+            const int u = tid + i * NT;
+            const int row = u / CH, c = u % CH;
+            *(u32x4 *)(ks + row * KP + 16 * c) = kreg[i];
+            *(u32x4 *)(vs + row * VP + 16 * c) = vreg[i];
+        }
+    };
+
+    const float c2 = a.scale_log2;
+
+    if (t_begin < t_end) {
+        load_tile(t_begin * KT);
+        store_tile(0);
+        __syncthreads();
+    }
+    for (int t = t_begin; t < t_end; ++t) {
+        const int buf = (t - t_begin) & 1;
+        const int kt = t * KT;
+        if (t + 1 < t_end) load_tile(kt + KT);
+        const char *ks = smem + buf * (KBYTES + VBYTES);
+        const char *vs = ks + KBYTES;
+
+        // S^T[key][query] = K Q^T for 64 keys x (32*NB) queries of this wave
+        f32x16 s[2][NB];
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int n = 0; n < NB; ++n)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) s[mb][n][v] = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb) {
+                const bf16x8 ka = *(const bf16x8 *)(ks + (mb * 32 + l32) * KP + (16 * kk + 8 * hf) * 2);
+#pragma unroll
+                for (int n = 0; n < NB; ++n)
+                    s[mb][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[n][kk], s[mb][n], 0, 0, 0);
+            }
+        }
+
+        // element masks only where the tile is not visible to every row
+        if (kt + KT > kfull) {
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int key = kt + mb * 32 + (v >> 2) * 8 + 4 * hf + (v & 3);
+#pragma unroll
+                    for (int n = 0; n < NB; ++n)
+                        if (key >= kend[n]) s[mb][n][v] = -INFINITY;
+                }
+        }
+
+        // online softmax (log2 domain)
+        bf16x8 pf[NB][4];
+#pragma unroll
+        for (int n = 0; n < NB; ++n) {
+            float mx = -INFINITY;
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[mb][n][v]);
+            mx = halves_max(mx);
+            const float m_new = fmaxf(m[n], mx * c2);
+            const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+            const float alpha = fast_exp2(m[n] - m_use);
+            m[n] = m_new;
+            float rs = 0.f;
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const float p = fast_exp2(__builtin_fmaf(s[mb][n][v], c2, -m_use));
+                    s[mb][n][v] = p;
+                    rs += p;
+                }
+            l[n] = l[n] * alpha + rs;
+#pragma unroll
+            for (int md = 0; md < MD; ++md)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) o[n][md][v] *= alpha;
+#pragma unroll
+            for (int ks4 = 0; ks4 < 4; ++ks4)
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    pf[n][ks4][e] = (__bf16)s[ks4 >> 1][n][8 * (ks4 & 1) + e];
+        }
+
+        // O^T[d][query] += V^T P^T; V^T fragments by LDS transpose reads
+        const int j16 = lane & 15;
+        const int dsub = 16 * ((lane >> 4) & 1) + 4 * (j16 & 3);
+#pragma unroll
+        for (int ks4 = 0; ks4 < 4; ++ks4) {
+            const int k0 = 16 * ks4 + 4 * hf + (j16 >> 2);
+#pragma unroll
+            for (int md = 0; md < MD; ++md) {
+                const int dcol = 32 * md + dsub;
+                const i16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_i16x4 *)(vs + k0 * VP + dcol * 2));
+                const i16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_i16x4 *)(vs + (k0 + 8) * VP + dcol * 2));
+                // whole-vector reinterpretation: element-wise bf16 casts of
+                // the transpose-read result were lowered to a splat
+                const bf16x8 vfrag = __builtin_bit_cast(
+                    bf16x8, __builtin_shufflevector(va, vb, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+                for (int n = 0; n < NB; ++n)
+                    o[n][md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag, pf[n][ks4], o[n][md], 0, 0, 0);
+            }
+        }
+
+        if (t + 1 < t_end) store_tile(buf ^ 1);
+        __syncthreads();
+    }
+
+    // ---- epilogue -------------------------------------------------------
+#pragma unroll
+    for (int n = 0; n < NB; ++n) {
+        const float lt = halves_sum(l[n]);
+        const int r = rows[n];
+        if (r >= a.Lq) continue;
+        if (a.nsplit == 1) {
+            const float inv = lt > 0.f ? 1.f / lt : 0.f;
+            if (a.out_f32) {
+                float *op = (float *)a.out + b * a.o_sb + (int64_t)r * a.o_st + hq * a.o_sh;
+#pragma unroll
+                for (int md = 0; md < MD; ++md)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        f32x4 val;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) val[e] = o[n][md][4 * g + e] * inv;
+                        *(f32x4 *)(op + 32 * md + 8 * g + 4 * hf) = val;
+                    }
+            } else {
+                uint16_t *op = (uint16_t *)a.out + b * a.o_sb + (int64_t)r * a.o_st + hq * a.o_sh;
+#pragma unroll
+                for (int md = 0; md < MD; ++md)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        u32x2 val;
+                        val[0] = pack_bf16x2(o[n][md][4 * g + 0] * inv, o[n][md][4 * g + 1] * inv);
+                        val[1] = pack_bf16x2(o[n][md][4 * g + 2] * inv, o[n][md][4 * g + 3] * inv);
+                        *(u32x2 *)(op + 32 * md + 8 * g + 4 * hf) = val;
+                    }
+            }
+            if (a.lse && hf == 0)
+                a.lse[((int64_t)b * a.Hq + hq) * a.Lq + r] = (m[n] + __builtin_amdgcn_logf(lt)) * 0.69314718055994531f;
+        } else {
+            const int64_t prow = (((int64_t)split * a.B + b) * a.Hq + hq) * a.Lq + r;
+            float *op = a.part_o + prow * D;
+#pragma unroll
+            for (int md = 0; md < MD; ++md)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    f32x4 val;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) val[e] = o[n][md][4 * g + e];
+                    *(f32x4 *)(op + 32 * md + 8 * g + 4 * hf) = val;
+                }
+            if (hf == 0) {
+                a.part_ml[2 * prow + 0] = m[n];
+                a.part_ml[2 * prow + 1] = lt;
+            }
+        }
+    }
+}
+
+// Merge the KV-split partials of every query row: with per-split running
+// max m_s (log2 domain), sum l_s and unnormalised o_s,
+//   M = max_s m_s,  L = sum_s l_s 2^(m_s - M),  o = sum_s o_s 2^(m_s - M) / L.
+// Splits are visited in a fixed order, so the result is deterministic.
+template <int D>
+__global__ __launch_bounds__(256) void combine_kernel(const AttnArgs a) {
+    constexpr int TPR = D / 4;              // threads per row, 4 elements each
+    constexpr int RPB = 256 / TPR;          // rows per block
+    const int64_t nrows = (int64_t)a.B * a.Hq * a.Lq;
+    const int64_t row = (int64_t)blockIdx.x * RPB + threadIdx.x / TPR;
+    const int c4 = threadIdx.x % TPR;
+    if (row >= nrows) return;
+    const int r = (int)(row % a.Lq);
+    const int hq = (int)((row / a.Lq) % a.Hq);
+    const int b = (int)(row / ((int64_t)a.Lq * a.Hq));
+    float M = -INFINITY;
+    for (int s = 0; s < a.nsplit; ++s) M = fmaxf(M, a.part_ml[2 * ((int64_t)s * nrows + row)]);
+    const float Mu = (M == -INFINITY) ? 0.f : M;
+    float L = 0.f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < a.nsplit; ++s) {
+        const int64_t prow = (int64_t)s * nrows + row;
+        const float wgt = __builtin_amdgcn_exp2f(a.part_ml[2 * prow] - Mu);
+        L += a.part_ml[2 * prow + 1] * wgt;
+        const f32x4 ov = *(const f32x4 *)(a.part_o + prow * D + 4 * c4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[e] += ov[e] * wgt;
+    }
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+    if (a.out_f32) {
+        float *op = (float *)a.out + b * a.o_sb + (int64_t)r * a.o_st + hq * a.o_sh + 4 * c4;
+        f32x4 val;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) val[e] = acc[e] * inv;
+        *(f32x4 *)op = val;
+    } else {
+        uint16_t *op = (uint16_t *)a.out + b * a.o_sb + (int64_t)r * a.o_st + hq * a.o_sh + 4 * c4;
+        u32x2 val;
+        val[0] = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+        val[1] = pack_bf16x2(acc[2] * inv, acc[3] * inv);
+        *(u32x2 *)op = val;
+    }
+    if (a.lse && c4 == 0) a.lse[row] = (M + __builtin_amdgcn_logf(L)) * 0.69314718055994531f;
+}
+
+// Copy new tokens' K/V rows into their cache slots: one 16-byte chunk per
+// thread; consecutive threads walk one token row, so reads and writes are
+// contiguous 256-byte runs (head_dim 128).
+__global__ __launch_bounds__(256) void append_kernel(const AppendArgs a) {
+    const int CH = a.D / 8;
+    const int64_t total = (int64_t)a.Ln * a.Hkv * CH;
+    const int b = blockIdx.y;
+    for (int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x; u < total; u += (int64_t)gridDim.x * 256) {
+        const int c = (int)(u % CH);
+        const int h = (int)((u / CH) % a.Hkv);
+        const int t = (int)(u / ((int64_t)CH * a.Hkv));
+        const int pos = a.cache_lens[b] + t;
+        const int page = a.page_table[(int64_t)b * a.max_pages + (pos >> 6)];
+        const int64_t dst = (((int64_t)page * a.Hkv + h) * KT + (pos & 63)) * a.D + 8 * c;
+        *(u32x4 *)(a.kpool + dst) = *(const u32x4 *)(a.kn + b * a.kn_sb + (int64_t)t * a.kn_st + h * a.kn_sh + 8 * c);
+        *(u32x4 *)(a.vpool + dst) = *(const u32x4 *)(a.vn + b * a.vn_sb + (int64_t)t * a.vn_st + h * a.vn_sh + 8 * c);
+    }
+}
+
+template <int D, int NB, int NW>
+int launch_attn_t(const AttnArgs &a, hipStream_t st) {
+    const int grid = a.per_xcd * NUM_XCD;
+    hipLaunchKernelGGL((attn_kernel<D, NB, NW>), dim3(grid), dim3(NW * 64), 0, st, a);
+    return (int)hipGetLastError();
+}
+
+}  // namespace
+
+int launch_attention(const AttnArgs &a, int head_dim, TileShape shape, void *stream) {
+    hipStream_t st = (hipStream_t)stream;
+    if (head_dim == 128) {
+        if (shape.nb == 2 && shape.nw == 4) return launch_attn_t<128, 2, 4>(a, st);
+        if (shape.nb == 1 && shape.nw == 4) return launch_attn_t<128, 1, 4>(a, st);
+        if (shape.nb == 1 && shape.nw == 8) return launch_attn_t<128, 1, 8>(a, st);
+    } else if (head_dim == 64) {
+        if (shape.nb == 2 && shape.nw == 4) return launch_attn_t<64, 2, 4>(a, st);
+        if (shape.nb == 1 && shape.nw == 4) return launch_attn_t<64, 1, 4>(a, st);
+        if (shape.nb == 1 && shape.nw == 8) return launch_attn_t<64, 1, 8>(a, st);
+    }
+    return (int)hipErrorInvalidValue;
+}
+
+int launch_combine(const AttnArgs &a, int head_dim, void *stream) {
+    hipStream_t st = (hipStream_t)stream;
+    const int64_t nrows = (int64_t)a.B * a.Hq * a.Lq;
+    if (head_dim == 128) {
+        const int64_t grid = (nrows + 7) / 8;
+        hipLaunchKernelGGL(combine_kernel<128>, dim3((unsigned)grid), dim3(256), 0, st, a);
+    } else {
+        const int64_t grid = (nrows + 15) / 16;
+        hipLaunchKernelGGL(combine_kernel<64>, dim3((unsigned)grid), dim3(256), 0, st, a);
+    }
+    return (int)hipGetLastError();
+}
+
+int launch_append(const AppendArgs &a, void *stream) {
+    hipStream_t st = (hipStream_t)stream;
+    const int64_t total = (int64_t)a.Ln * a.Hkv * (a.D / 8);
+    int64_t gx = (total + 255) / 256;
+    if (gx > 4096) gx = 4096;
+    if (gx < 1) gx = 1;
+    hipLaunchKernelGGL(append_kernel, dim3((unsigned)gx, (unsigned)a.B), dim3(256), 0, st, a);
+    return (int)hipGetLastError();
+}
+
+}  // namespace ws

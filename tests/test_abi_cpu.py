@@ -1,0 +1,193 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/ws_attn.h declares, and rejects bad arguments with the documented
+status before touching any device memory (all "device" pointers below are
+fake and never dereferenced, because validation fails first)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2606_25041_amd as ws
+from paper_2606_25041_amd import build as wsbuild
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ws_attn.h")
+FAKE = 0x10000  # 16-byte aligned, never dereferenced
+
+
+# Every call below must fail validation: the pointers are fake, so a call
+# that passed would launch a kernel on them.  Never run this module where a
+# GPU is visible.
+if torch.cuda.device_count() > 0:
+    pytest.skip("uses fake device pointers; CPU-only module", allow_module_level=True)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(wsbuild.LIB):
+        wsbuild.build()
+    return ws.library()
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ws_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = header_functions()
+    assert {"ws_kv_append", "ws_block_causal_attn_fwd", "ws_block_causal_prefill",
+            "ws_workspace_bytes", "ws_abi_version", "ws_status_string", "ws_last_error"} <= set(names)
+    for name in names:
+        assert hasattr(lib, name), name
+    assert lib.ws_abi_version() == 1
+    assert lib.ws_status_string(0) == b"WS_OK"
+    assert lib.ws_status_string(10) == b"WS_ERR_HIP"
+
+
+def t4(ptr=FAKE, dtype=ws.WS_DTYPE_BF16, sb=0, st=0, sh=0, d=128, L=16, H=4):
+    if sb == 0 and st == 0 and sh == 0:
+        sh, st, sb = d, H * d, L * H * d
+    return ws.Tensor4(ptr, dtype, sb, st, sh)
+
+
+class Host:
+    """Host arrays the library validates (kept alive by this object)."""
+
+    def __init__(self, B=2, max_pages=4, num_pages=10, lens=(10, 100)):
+        self.table = np.arange(B * max_pages, dtype=np.int32).reshape(B, max_pages) % num_pages
+        self.lens = np.array(lens, dtype=np.int32)
+        self.num_pages, self.max_pages = num_pages, max_pages
+
+    def desc(self, **kw):
+        d = dict(k_pool=FAKE, v_pool=FAKE, page_table_dev=FAKE,
+                 page_table_host=self.table.ctypes.data, num_pages=self.num_pages,
+                 page_size=64, max_pages_per_seq=self.max_pages, num_kv_heads=2, head_dim=128)
+        d.update(kw)
+        return ws.PagedKVDesc(**d)
+
+
+def step_call(lib, h, desc=None, q=None, kn=None, vn=None, out=None, B=2, Lq=16, Hq=4,
+              scale=0.088, flags=0, lse=None, wsp=FAKE, wsb=1 << 30, lens_ptr="host"):
+    desc = desc or h.desc()
+    q = q or t4(H=Hq, L=Lq)
+    kn = kn or t4(H=2, L=Lq)
+    vn = vn or t4(H=2, L=Lq)
+    out = out or t4(H=Hq, L=Lq)
+    lh = h.lens.ctypes.data if lens_ptr == "host" else lens_ptr
+    return lib.ws_block_causal_attn_fwd(q, kn, vn, ctypes.byref(desc), lh, FAKE, B, Lq, Hq,
+                                        scale, flags, out, lse, wsp, wsb, None)
+
+
+def test_step_errors(lib):
+    h = Host()
+    assert step_call(lib, h, q=t4(ptr=None)) == 1                      # NULL q
+    assert step_call(lib, h, lens_ptr=None) == 1                       # NULL cache_lens
+    assert step_call(lib, h, desc=h.desc(k_pool=None)) == 1            # NULL pool
+    assert step_call(lib, h, desc=h.desc(page_table_host=None)) == 1   # NULL host table
+    assert step_call(lib, h, B=-1) == 2                                # negative batch
+    assert step_call(lib, h, Hq=0) == 2
+    assert step_call(lib, h, desc=h.desc(head_dim=96)) == 3            # head_dim
+    assert step_call(lib, h, desc=h.desc(page_size=32)) == 3           # page size
+    assert step_call(lib, h, q=t4(dtype=ws.WS_DTYPE_F32)) == 3         # f32 input
+    assert step_call(lib, h, flags=4) == 3                             # unknown flag
+    assert step_call(lib, h, scale=0.0) == 3
+    assert step_call(lib, h, scale=float("nan")) == 3
+    assert step_call(lib, h, q=t4(ptr=FAKE + 2)) == 4                  # misaligned pointer
+    assert step_call(lib, h, q=t4(sb=16 * 4 * 128, st=4 * 128, sh=130)) == 4  # stride % 8
+    assert step_call(lib, h, lse=FAKE + 2) == 4
+    assert step_call(lib, h, Hq=3, q=t4(H=3), out=t4(H=3)) == 8        # Hq % Hkv
+    h2 = Host(lens=(10, 300))                                          # 300 > 4 pages * 64
+    assert step_call(lib, h2) == 7
+    h4 = Host()
+    h4.table[1, 1] = 99                                                # page id out of range
+    assert step_call(lib, h4) == 6
+    h5 = Host(lens=(10, -1))
+    assert step_call(lib, h5) == 2
+    hw = Host(lens=(10, 200))            # 216 keys: the plan splits the KV range
+    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 2, 4, 16, 216) > 0
+    assert step_call(lib, hw, wsp=None) == 9
+    assert step_call(lib, hw, wsb=16) == 9
+    assert step_call(lib, hw, wsp=FAKE + 4) == 9                       # misaligned workspace
+    assert lib.ws_last_error() != b""
+
+
+def test_step_capacity_counts_fused_append(lib):
+    # cache of 250 tokens fits 4 pages, but committing 16 more does not
+    h = Host(lens=(10, 250))
+    assert step_call(lib, h, flags=ws.WS_FUSE_APPEND) == 7
+    h.table[1, 3] = -5  # the 4th page is only read for the append
+    assert step_call(lib, h, flags=ws.WS_FUSE_APPEND) in (6, 7)
+
+
+def append_call(lib, h, desc=None, B=2, Ln=16, kn=None, vn=None, lens_ptr="host"):
+    desc = desc or h.desc()
+    lh = h.lens.ctypes.data if lens_ptr == "host" else lens_ptr
+    return lib.ws_kv_append(ctypes.byref(desc), B, lh, FAKE, Ln, kn or t4(H=2, L=Ln),
+                            vn or t4(H=2, L=Ln), None)
+
+
+def test_append_errors(lib):
+    h = Host()
+    assert append_call(lib, h, lens_ptr=None) == 1
+    assert append_call(lib, h, kn=t4(ptr=None)) == 1
+    assert append_call(lib, h, B=-2) == 2
+    assert append_call(lib, h, Ln=-1) == 2
+    assert append_call(lib, h, desc=h.desc(head_dim=32)) == 3
+    assert append_call(lib, h, kn=t4(ptr=FAKE + 8)) == 4
+    assert append_call(lib, h, Ln=200) == 7          # 100 + 200 > 256
+    h.table[0, 0] = 10                               # == num_pages
+    assert append_call(lib, h) == 6
+
+
+def prefill_call(lib, offs, B=1, L=None, nb=None, Hq=4, Hkv=2, d=128, q=None, k=None, v=None,
+                 out=None, desc=None, scale=0.1):
+    offs = np.ascontiguousarray(np.asarray(offs, np.int32))
+    L = int(offs.reshape(B, -1)[0, -1]) if L is None else L
+    nb = offs.reshape(B, -1).shape[1] - 1 if nb is None else nb
+    q = q or t4(H=Hq, L=L, d=d)
+    k = k if k is not None else t4(H=Hkv, L=L, d=d)
+    v = v if v is not None else t4(H=Hkv, L=L, d=d)
+    out = out or t4(H=Hq, L=L, d=d)
+    return lib.ws_block_causal_prefill(q, k, v, ctypes.byref(desc) if desc else None,
+                                       offs.ctypes.data, FAKE, B, L, nb, Hq, Hkv, d, scale, out,
+                                       None, None)
+
+
+def test_prefill_errors(lib):
+    assert prefill_call(lib, [[1, 5, 9]]) == 5                    # first offset != 0
+    assert prefill_call(lib, [[0, 6, 5, 9]]) == 5                 # decreasing
+    assert prefill_call(lib, [[0, 5, 9]], L=10) == 5              # last != seq_len
+    assert prefill_call(lib, [[0, 4, 8], [0, 2, 7]], B=2, L=8) == 5
+    assert prefill_call(lib, [[0, 8]], Hq=6, Hkv=4) == 8
+    assert prefill_call(lib, [[0, 8]], d=80) == 3
+    assert prefill_call(lib, [[0, 8]], q=t4(ptr=None)) == 1
+    null = ws.Tensor4(None, 1, 0, 0, 0)
+    assert prefill_call(lib, [[0, 8]], k=null, v=null) == 1       # paged without a cache
+    assert prefill_call(lib, [[0, 8]], Hq=0) == 2
+    h = Host(B=1, lens=(0,))
+    assert prefill_call(lib, [[0, 300]], k=null, v=null, desc=h.desc()) == 7
+    h.table[0, 2] = 77
+    assert prefill_call(lib, [[0, 150]], k=null, v=null, desc=h.desc()) == 6
+    assert prefill_call(lib, [[0, 150]], k=null, v=null, desc=h.desc(num_kv_heads=4)) == 8
+
+
+def test_empty_calls_are_ok(lib):
+    h = Host(B=0, lens=())
+    assert step_call(lib, h, B=0) == 0
+    assert prefill_call(lib, [[0]], L=0, nb=0) == 0
+    assert prefill_call(lib, np.zeros((0, 3), np.int32), B=0, L=5, nb=2) == 0
+
+
+def test_workspace_bytes(lib):
+    # a single 256-row tile per head needs KV splits (and partials) to fill the chip
+    n = lib.ws_workspace_bytes(ws.WS_OP_STEP, 1, 24, 256, 4352)
+    assert n > 0 and n % (24 * 256 * 130 * 4) == 0
+    # enough work items already: no splits, no workspace
+    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 4, 64, 512, 131584) == 0
+    assert lib.ws_workspace_bytes(ws.WS_OP_PREFILL, 2, 32, 16384, 16384) == 0
+    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 0, 24, 256, 4352) == 0

@@ -1,0 +1,130 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle,
+element by element on seeded inputs.  Small cases span several 64-key tiles,
+several query tiles and ragged tails; the five named workloads run at full
+size and are checked on sampled rows that the oracle computes one by one.
+Tolerance: max-abs 2e-2, mean-abs 2e-3 (bf16 outputs), lse 1e-3."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_25041_amd import inputs
+from tests import gpu_support as gs
+
+pytestmark = pytest.mark.gpu
+
+
+def _prefill_case(name, B, Hq, Hkv, D, L, nb, seed, paged=False, out_f32=False):
+    g = np.random.default_rng([seed, 99])
+    lens = []
+    for _ in range(B):
+        cuts = np.sort(g.choice(np.arange(1, L), size=nb - 1, replace=False))
+        lens.append(np.diff(np.concatenate([[0], cuts, [L]])))
+    return inputs.prefill_workload(name, B, Hq, Hkv, D, lens, seed, paged=paged, out_f32=out_f32)
+
+
+def _check_full(wl, cache=None, **kw):
+    gs.say(f"[gpu] {wl.name}: B={wl.B} Hq={wl.Hq} Hkv={wl.Hkv} D={wl.D} Lq={wl.Lq}")
+    out, lse = gs.run_gpu(wl, cache=cache, **kw)
+    torch.cuda.synchronize()
+    ref, ref_lse = gs.run_oracle(wl)
+    stats = gs.compare(out, lse, ref, ref_lse)
+    gs.assert_close(stats)
+    return out, lse, stats
+
+
+def test_tiny_config_full():
+    wl = inputs.config(1)
+    out, _, stats = _check_full(wl)
+    assert out.dtype == torch.float32
+
+
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("L,nb", [(777, 9), (100, 3), (1300, 40)])
+def test_prefill_contiguous_ragged(D, L, nb):
+    wl = _prefill_case(f"prefill_c_d{D}_L{L}", 2, 4, 2, D, L, nb, seed=7 + L + D)
+    _check_full(wl)
+
+
+def test_prefill_unit_and_empty_blocks():
+    # blocks of length 1 (token-causal stretch), empty blocks, one long block
+    lens = [np.array([1, 1, 1, 0, 5, 0, 1, 200, 1, 1, 0, 90])]
+    wl = inputs.prefill_workload("prefill_unit_empty", 1, 2, 1, 128, lens, 31)
+    _check_full(wl)
+
+
+def test_prefill_single_block_and_f32_out():
+    wl = inputs.prefill_workload("prefill_single_block", 1, 2, 2, 128, [np.array([700])], 32,
+                                 out_f32=True)
+    _check_full(wl)
+
+
+def test_prefill_paged_interleaved():
+    g = inputs.rng(41, inputs.S_LENGTHS)
+    lens = inputs.interleaved_block_lengths(g, 10)
+    wl = inputs.prefill_workload("prefill_paged_interleaved", 1, 5, 1, 128, [lens], 41, paged=True)
+    cache = gs.device_cache(wl, [wl.Lq])
+    _check_full(wl, cache=cache)
+
+
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("Lq,lens", [(100, [0, 333, 64]), (1, [5, 700, 64]), (300, [129, 0, 1000])])
+def test_step_ragged(D, Lq, lens):
+    wl = inputs.step_workload(f"step_d{D}_q{Lq}", 3, 8, 2, D, Lq, lens, seed=11 + Lq + D)
+    cache = gs.device_cache(wl, wl.cache_lens)
+    _check_full(wl, cache=cache)
+
+
+def test_step_mha_f32_out():
+    wl = inputs.step_workload("step_mha_f32", 1, 6, 6, 128, 256, [1000], seed=13)
+    cache = gs.device_cache(wl, wl.cache_lens)
+    _check_full(wl, cache=cache, out_dtype=torch.float32)
+
+
+# ---------------------------------------------------------------------------
+# the five named workloads at full size (sampled rows)
+
+def _sampled(wl, cache, must, n=48, seed=5):
+    g = np.random.default_rng(seed)
+    rows = inputs.sample_rows(g, wl.B, wl.Hq, wl.Lq, n, must=must)
+    gs.say(f"[gpu] {wl.name}: full size, {len(rows)} sampled rows")
+    out, lse = gs.run_gpu(wl, cache=cache)
+    torch.cuda.synchronize()
+    ref, ref_lse = gs.run_oracle(wl, rows=rows)
+    stats = gs.compare(out, lse, ref, ref_lse, rows=rows)
+    gs.assert_close(stats)
+    # every output finite (no NaN from unused pool pages)
+    assert torch.isfinite(out).all()
+    return stats
+
+
+def test_config2_step_full_size():
+    wl = inputs.config(2)
+    cache = gs.device_cache(wl, wl.cache_lens, fill_on_gpu=True)
+    _sampled(wl, cache, must=[(0, 0, 0), (0, 23, 255), (0, 11, 128), (0, 5, 63)])
+
+
+def test_config3_prefill_full_size():
+    wl = inputs.config(3)
+    _sampled(wl, None, must=[(0, 0, 0), (1, 31, 16383), (0, 7, 255), (1, 8, 256), (0, 16, 8191)])
+
+
+def test_config4_interleaved_full_size():
+    wl = inputs.config(4)
+    cache = gs.device_cache(wl, [wl.Lq], fill_on_gpu=True)
+    offs = wl.offsets[0]
+    must = [(0, 0, int(offs[j])) for j in (1, 50, 127)] + [(0, 39, int(offs[j]) - 1) for j in (2, 64, 128)]
+    _sampled(wl, cache, must=must)
+
+
+def test_config5_streams_full_size():
+    wl = inputs.config(5)
+    cache = gs.device_cache(wl, wl.cache_lens, fill_on_gpu=True)
+    must = [(0, 0, 0), (3, 63, 511), (1, 8, 256), (2, 7, 255)]
+    _sampled(wl, cache, must=must, n=24)
+    # the fused append committed the new block at positions 131072 ..
+    kn = wl.k_new
+    for b, t in [(0, 0), (3, 511), (2, 300)]:
+        pos = int(wl.cache_lens[b]) + t
+        page = int(wl.page_table[b][pos // 64])
+        got = cache.k_pool[page, :, pos % 64].cpu()
+        assert torch.equal(got.view(torch.int16), kn[b, t].view(torch.int16))
