@@ -95,20 +95,30 @@ struct StepPlan {
 };
 
 // Query tile and KV split count of a streaming step.  Splits are added only
-// until about one work-group per CU exists, and every split keeps at least
-// two 64-key tiles.
+// while the work-groups still fit one round on the CUs, and every split
+// keeps at least two 64-key tiles.
+// Tuning override: WS_SHAPE=<32-query blocks per wave><waves per group>,
+// e.g. "24" (2 blocks x 4 waves), "14", "18".
+bool shape_override(ws::TileShape &s) {
+    const int v = env_int("WS_SHAPE", 0);
+    const ws::TileShape c{v / 10, v % 10};
+    if ((c.nb == 2 && c.nw == 4) || (c.nb == 1 && c.nw == 4) || (c.nb == 1 && c.nw == 8)) {
+        s = c;
+        return true;
+    }
+    return false;
+}
+
 StepPlan plan_step(int batch, int hq, int lq, int64_t max_k) {
     StepPlan p;
-    const int qt_env = env_int("WS_QTILE", 0);
-    if (qt_env == 128) p.shape = {1, 4};
-    else if (qt_env == 256) p.shape = {2, 4};
-    else p.shape = (lq >= 256) ? ws::TileShape{2, 4} : ws::TileShape{1, 4};
+    if (!shape_override(p.shape)) p.shape = (lq > 128) ? ws::TileShape{1, 8} : ws::TileShape{1, 4};
     const int qt = p.shape.qtile();
     p.nqt = (lq + qt - 1) / qt;
     const int64_t base = (int64_t)batch * hq * p.nqt;
     const int64_t ntiles = (max_k + 63) / 64;
     int64_t ns = 1;
-    if (base > 0 && base < TARGET_WORKGROUPS) ns = (TARGET_WORKGROUPS + base - 1) / base;
+    // the largest split count that still fits one round of work-groups
+    if (base > 0 && base < TARGET_WORKGROUPS) ns = TARGET_WORKGROUPS / base;
     if (ns > ntiles / 2) ns = ntiles / 2;
     if (ns > WS_MAX_SPLITS) ns = WS_MAX_SPLITS;
     if (ns < 1) ns = 1;
@@ -124,10 +134,9 @@ size_t step_workspace(const StepPlan &p, int batch, int hq, int lq) {
 }
 
 ws::TileShape plan_prefill(int seq_len) {
-    const int qt_env = env_int("WS_QTILE", 0);
-    if (qt_env == 128) return {1, 4};
-    if (qt_env == 256) return {2, 4};
-    return seq_len >= 512 ? ws::TileShape{2, 4} : ws::TileShape{1, 4};
+    ws::TileShape s;
+    if (shape_override(s)) return s;
+    return seq_len > 128 ? ws::TileShape{1, 8} : ws::TileShape{1, 4};
 }
 
 // Total work items; fails when the grid would not fit the kernel's int math.

@@ -48,6 +48,7 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int KT = 64;        // keys per tile (= page size)
 constexpr int NUM_XCD = 8;    // MI355X: 8 XCDs, work-groups dispatched round-robin
+constexpr float RESCALE_LOG2 = 8.f;  // lazy-rescale threshold (log2 units)
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
@@ -178,35 +179,66 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     }
 
     // ---- tile staging ---------------------------------------------------
+    // Physical page of a tile, read one tile ahead of its K/V loads so the
+    // dependent page-table load does not sit in front of them.
+    auto page_of = [&](int t) -> int {
+        return (t < t_end && t * KT < n_pool) ? a.page_table[(int64_t)b * a.max_pages + t] : 0;
+    };
+    // Per-thread parts of the K/V addresses, fixed for the whole loop: this
+    // thread stages chunk c of rows row0 + i * (NT / CH) of every tile.
+    constexpr int RSTEP = NT / CH;
+    const int row0 = tid / CH;
+    const int cchunk = tid % CH;
+    const int64_t page_elems = (int64_t)a.Hkv * KT * D;
+    const uint16_t *kpool_t = a.kpool + ((int64_t)kvh * KT + row0) * D + 8 * cchunk;
+    const uint16_t *vpool_t = a.vpool + ((int64_t)kvh * KT + row0) * D + 8 * cchunk;
+    const uint16_t *kc_t = a.kc + b * a.kc_sb + kvh * a.kc_sh + 8 * cchunk;
+    const uint16_t *vc_t = a.vc + b * a.vc_sb + kvh * a.vc_sh + 8 * cchunk;
     u32x4 kreg[LOADS], vreg[LOADS];
+    int page_next = page_of(t_begin);
     auto load_tile = [&](int kt) {
-        int page = 0;
-        if (kt < n_pool) page = a.page_table[(int64_t)b * a.max_pages + (kt >> 6)];
+        const int page = page_next;
+        page_next = page_of((kt >> 6) + 1);
+        if (kt + KT <= n_pool) {
+            // whole tile in one cache page
+            const int64_t po = (int64_t)page * page_elems;
 #pragma unroll
-        for (int i = 0; i < LOADS; ++i) {
-            const int u = tid + i * NT;
-            const int row = u / CH, c = u % CH;
-            const int j = min(kt + row, k_hi - 1);  // past the end: repeat a valid row (masked)
-            if (j < n_pool) {
-                const int64_t off = (((int64_t)page * a.Hkv + kvh) * KT + (j & 63)) * D + 8 * c;
-                kreg[i] = *(const u32x4 *)(a.kpool + off);
-                vreg[i] = *(const u32x4 *)(a.vpool + off);
-            } else {
-                const int jj = j - n_pool;
-                kreg[i] = *(const u32x4 *)(a.kc + b * a.kc_sb + (int64_t)jj * a.kc_st + kvh * a.kc_sh + 8 * c);
-                vreg[i] = *(const u32x4 *)(a.vc + b * a.vc_sb + (int64_t)jj * a.vc_st + kvh * a.vc_sh + 8 * c);
+            for (int i = 0; i < LOADS; ++i) {
+                kreg[i] = *(const u32x4 *)(kpool_t + po + i * RSTEP * D);
+                vreg[i] = *(const u32x4 *)(vpool_t + po + i * RSTEP * D);
+            }
+        } else if (kt >= n_pool && kt + KT <= k_hi) {
+            // whole tile in the contiguous keys
+            const int64_t j0 = kt - n_pool + row0;
+#pragma unroll
+            for (int i = 0; i < LOADS; ++i) {
+                kreg[i] = *(const u32x4 *)(kc_t + (j0 + i * RSTEP) * a.kc_st);
+                vreg[i] = *(const u32x4 *)(vc_t + (j0 + i * RSTEP) * a.vc_st);
+            }
+        } else {
+            // the tile straddles the cache end or runs past the last key:
+            // rows past the end repeat a valid row (their scores are masked)
+#pragma unroll
+            for (int i = 0; i < LOADS; ++i) {
+                const int j = min(kt + row0 + i * RSTEP, k_hi - 1);
+                if (j < n_pool) {
+                    const int64_t po = (int64_t)page * page_elems + (int64_t)((j & 63) - row0) * D;
+                    kreg[i] = *(const u32x4 *)(kpool_t + po);
+                    vreg[i] = *(const u32x4 *)(vpool_t + po);
+                } else {
+                    kreg[i] = *(const u32x4 *)(kc_t + (int64_t)(j - n_pool) * a.kc_st);
+                    vreg[i] = *(const u32x4 *)(vc_t + (int64_t)(j - n_pool) * a.vc_st);
+                }
             }
         }
     };
     auto store_tile = [&](int buf) {
-        char *ks = smem + buf * (KBYTES + VBYTES);
-        char *vs = ks + KBYTES;
+        char *ks = smem + buf * (KBYTES + VBYTES) + row0 * KP + 16 * cchunk;
+        char *vs = smem + buf * (KBYTES + VBYTES) + KBYTES + row0 * VP + 16 * cchunk;
 #pragma unroll
         for (int i = 0; i < LOADS; ++i) {
-            const int u = tid + i * NT;
-            const int row = u / CH, c = u % CH;
-            *(u32x4 *)(ks + row * KP + 16 * c) = kreg[i];
-            *(u32x4 *)(vs + row * VP + 16 * c) = vreg[i];
+            *(u32x4 *)(ks + i * RSTEP * KP) = kreg[i];
+            *(u32x4 *)(vs + i * RSTEP * VP) = vreg[i];
         }
     };
 
@@ -265,11 +297,24 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
             for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[mb][n][v]);
-            mx = halves_max(mx);
-            const float m_new = fmaxf(m[n], mx * c2);
-            const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-            const float alpha = fast_exp2(m[n] - m_use);
-            m[n] = m_new;
+            mx = halves_max(mx) * c2;
+            // Lazy rescale: the running max m only moves when the tile max
+            // exceeds it by more than 2^RESCALE_LOG2, so most tiles skip the
+            // rescale of O and l (a wave-uniform branch).  Weights stay
+            // <= 2^RESCALE_LOG2; O and l share the same m, so the final
+            // quotient is unchanged.
+            const bool grow = mx > m[n] + RESCALE_LOG2;
+            if (__builtin_amdgcn_ballot_w64(grow)) {
+                const float m_new = grow ? mx : m[n];
+                const float alpha = fast_exp2(m[n] - m_new);  // 1 where m is kept; 0 from -inf
+                m[n] = m_new;
+                l[n] *= alpha;
+#pragma unroll
+                for (int md = 0; md < MD; ++md)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) o[n][md][v] *= alpha;
+            }
+            const float m_use = (m[n] == -INFINITY) ? 0.f : m[n];
             float rs = 0.f;
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb)
@@ -279,11 +324,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
                     s[mb][n][v] = p;
                     rs += p;
                 }
-            l[n] = l[n] * alpha + rs;
-#pragma unroll
-            for (int md = 0; md < MD; ++md)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) o[n][md][v] *= alpha;
+            l[n] += rs;
 #pragma unroll
             for (int ks4 = 0; ks4 < 4; ++ks4)
 #pragma unroll
@@ -374,7 +415,9 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
 // Merge the KV-split partials of every query row: with per-split running
 // max m_s (log2 domain), sum l_s and unnormalised o_s,
 //   M = max_s m_s,  L = sum_s l_s 2^(m_s - M),  o = sum_s o_s 2^(m_s - M) / L.
-// Splits are visited in a fixed order, so the result is deterministic.
+// Splits are visited in a fixed order, so the result is deterministic.  One
+// thread owns 4 elements of a row; the split loops are unrolled so their
+// independent loads are in flight together.
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(const AttnArgs a) {
     constexpr int TPR = D / 4;              // threads per row, 4 elements each
@@ -386,16 +429,21 @@ __global__ __launch_bounds__(256) void combine_kernel(const AttnArgs a) {
     const int r = (int)(row % a.Lq);
     const int hq = (int)((row / a.Lq) % a.Hq);
     const int b = (int)(row / ((int64_t)a.Lq * a.Hq));
+    const int S = a.nsplit;
+    const float2 *ml = (const float2 *)a.part_ml + row;
     float M = -INFINITY;
-    for (int s = 0; s < a.nsplit; ++s) M = fmaxf(M, a.part_ml[2 * ((int64_t)s * nrows + row)]);
+#pragma unroll 8
+    for (int s = 0; s < S; ++s) M = fmaxf(M, ml[(int64_t)s * nrows].x);
     const float Mu = (M == -INFINITY) ? 0.f : M;
     float L = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < a.nsplit; ++s) {
-        const int64_t prow = (int64_t)s * nrows + row;
-        const float wgt = __builtin_amdgcn_exp2f(a.part_ml[2 * prow] - Mu);
-        L += a.part_ml[2 * prow + 1] * wgt;
-        const f32x4 ov = *(const f32x4 *)(a.part_o + prow * D + 4 * c4);
+    const float *po = a.part_o + row * D + 4 * c4;
+#pragma unroll 8
+    for (int s = 0; s < S; ++s) {
+        const float2 mls = ml[(int64_t)s * nrows];
+        const f32x4 ov = *(const f32x4 *)(po + (int64_t)s * nrows * D);
+        const float wgt = __builtin_amdgcn_exp2f(mls.x - Mu);
+        L += mls.y * wgt;
 #pragma unroll
         for (int e = 0; e < 4; ++e) acc[e] += ov[e] * wgt;
     }
