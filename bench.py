@@ -182,15 +182,18 @@ def cpu_baseline(wl):
 
 
 def load_traffic(workload_name):
-    """HBM bytes per launch measured with rocprofv3 counters (FETCH_SIZE,
-    WRITE_SIZE), if a summary for the current kernel source exists."""
-    p = os.path.join(ROOT, "profiles", f"traffic_{workload_name}.json")
+    """HBM bytes per step measured with rocprofv3 counters (FETCH_SIZE and
+    WRITE_SIZE, scaled by a copy-kernel calibration), if the committed summary
+    was taken on the current kernel source; None otherwise."""
+    p = os.path.join(ROOT, "profiles", f"traffic_attn_{workload_name}.txt")
     if not os.path.exists(p):
         return None
-    d = json.load(open(p))
-    if d.get("kernel_source_hash") != kernel_source_hash():
-        return None
-    return d.get("bytes_per_launch")
+    for line in open(p):
+        if line.startswith("machine-readable:"):
+            d = json.loads(line.split(":", 1)[1])
+            if d.get("kernel_source_hash") == kernel_source_hash():
+                return d.get("bytes_per_launch")
+    return None
 
 
 def main():
@@ -201,7 +204,20 @@ def main():
     ap.add_argument("--no-extra", action="store_true", help="headline workload only")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--config", type=int, default=2, help="headline workload index (1-5)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB five times (to calibrate "
+                         "the FETCH_SIZE / WRITE_SIZE counters against known bytes)")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n, "copies": 5}), flush=True)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(see the sharding notes in DESIGN.md); run with --gpus 1", file=sys.stderr)

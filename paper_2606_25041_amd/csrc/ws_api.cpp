@@ -29,7 +29,7 @@ int ok() {
     return WS_OK;
 }
 
-constexpr int TARGET_WORKGROUPS = 256;  // one wave of work-groups on 256 CUs
+constexpr int NUM_CUS = 256;            // MI355X compute units
 constexpr int WS_MAX_SPLITS = 32;
 constexpr int WS_MAX_HEAD_DIM = 128;
 
@@ -98,11 +98,11 @@ struct StepPlan {
 // while the work-groups still fit one round on the CUs, and every split
 // keeps at least two 64-key tiles.
 // Tuning override: WS_SHAPE=<32-query blocks per wave><waves per group>,
-// e.g. "24" (2 blocks x 4 waves), "14", "18".
+// "14" or "18".
 bool shape_override(ws::TileShape &s) {
     const int v = env_int("WS_SHAPE", 0);
     const ws::TileShape c{v / 10, v % 10};
-    if ((c.nb == 2 && c.nw == 4) || (c.nb == 1 && c.nw == 4) || (c.nb == 1 && c.nw == 8)) {
+    if (c.nb == 1 && (c.nw == 4 || c.nw == 8)) {
         s = c;
         return true;
     }
@@ -116,9 +116,10 @@ StepPlan plan_step(int batch, int hq, int lq, int64_t max_k) {
     p.nqt = (lq + qt - 1) / qt;
     const int64_t base = (int64_t)batch * hq * p.nqt;
     const int64_t ntiles = (max_k + 63) / 64;
+    const int64_t slots = (int64_t)NUM_CUS * p.shape.groups_per_cu();
     int64_t ns = 1;
     // the largest split count that still fits one round of work-groups
-    if (base > 0 && base < TARGET_WORKGROUPS) ns = TARGET_WORKGROUPS / base;
+    if (base > 0 && base < slots) ns = slots / base;
     if (ns > ntiles / 2) ns = ntiles / 2;
     if (ns > WS_MAX_SPLITS) ns = WS_MAX_SPLITS;
     if (ns < 1) ns = 1;
@@ -128,9 +129,11 @@ StepPlan plan_step(int batch, int hq, int lq, int64_t max_k) {
     return p;
 }
 
+// Partials are kept in blocks of 32 query rows.
 size_t step_workspace(const StepPlan &p, int batch, int hq, int lq) {
     if (p.nsplit <= 1) return 0;
-    return (size_t)p.nsplit * batch * hq * lq * (WS_MAX_HEAD_DIM + 2) * sizeof(float);
+    const size_t rows = (size_t)(lq + 31) / 32 * 32;
+    return (size_t)p.nsplit * batch * hq * rows * (WS_MAX_HEAD_DIM + 2) * sizeof(float);
 }
 
 ws::TileShape plan_prefill(int seq_len) {
@@ -259,9 +262,14 @@ int ws_block_causal_attn_fwd(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, c
     a.nsplit = plan.nsplit;
     a.nqt = plan.nqt;
     a.scale_log2 = scale * 1.4426950408889634f;
+    a.nrb = (new_len + 31) / 32;
     if (plan.nsplit > 1) {
         a.part_o = (float *)workspace;
-        a.part_ml = a.part_o + (size_t)plan.nsplit * batch * num_q_heads * new_len * kv->head_dim;
+        a.part_ml = a.part_o + (size_t)plan.nsplit * batch * num_q_heads * a.nrb * 32 * kv->head_dim;
+    }
+    if (batch <= ws::LENS_IN_ARGS) {
+        a.lens_in_args = 1;
+        for (int b = 0; b < batch; ++b) a.lens_arg[b] = cache_lens_host[b];
     }
     if (!finish_work(a)) return fail(WS_ERR_SHAPE, "too many work items");
     if (int e = ws::launch_attention(a, kv->head_dim, plan.shape, stream))

@@ -31,8 +31,11 @@ struct AttnArgs {
     int64_t o_sb, o_st, o_sh;
     int32_t out_f32;
     float *lse;
-    // split-KV partials: o [S][B][Hq][Lq][D] f32, (m, l) [S][B][Hq][Lq][2]
+    // split-KV partials, in blocks of 32 query rows (nrb = ceil(Lq / 32)
+    // blocks per (b, hq)): o [S][B][Hq][nrb][D/4][64 lanes][4] f32 in the
+    // accumulator's register order; (m, l) [S][B][Hq][nrb * 32][2]
     float *part_o, *part_ml;
+    int32_t nrb;
     int32_t B, Lq, Hq, Hkv, G;
     int32_t mode;        // MODE_PREFILL or MODE_STEP
     int32_t paged;       // prefill only: keys/values come from the pool
@@ -42,7 +45,13 @@ struct AttnArgs {
     int32_t n_work;      // B * Hq * nqt * nsplit
     int32_t per_xcd;     // ceil(n_work / 8)
     float scale_log2;    // scale * log2(e)
+    // step: cache lengths also passed by value when batch <= LENS_IN_ARGS,
+    // so the first page lookup does not wait on a load of them
+    int32_t lens_in_args;
+    int32_t lens_arg[32];
 };
+
+constexpr int LENS_IN_ARGS = 32;
 
 struct AppendArgs {
     const uint16_t *kn, *vn;
@@ -60,6 +69,8 @@ struct TileShape {
     int nb;  // 32-query column blocks per wave
     int nw;  // waves per work-group
     int qtile() const { return nb * nw * 32; }
+    // work-groups resident per CU (LDS and registers allow one)
+    int groups_per_cu() const { return 1; }
 };
 
 // Each returns 0 or a HIP error code (hipError_t as int).

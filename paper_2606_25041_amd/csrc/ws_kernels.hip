@@ -49,6 +49,7 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int KT = 64;        // keys per tile (= page size)
 constexpr int NUM_XCD = 8;    // MI355X: 8 XCDs, work-groups dispatched round-robin
 constexpr float RESCALE_LOG2 = 8.f;  // lazy-rescale threshold (log2 units)
+constexpr int PAGE_LDS = 2560;       // page ids of a split staged in LDS (more: read from memory)
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
@@ -93,6 +94,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     constexpr int MD = D / 32;            // 32-row blocks of head_dim for O^T
     static_assert((KT * CH) % NT == 0, "tile chunks must divide among threads");
     __shared__ __attribute__((aligned(16))) char smem[2 * (KBYTES + VBYTES)];
+    __shared__ int page_lds[PAGE_LDS];
 
     // ---- work item ------------------------------------------------------
     const int bid = blockIdx.x;
@@ -122,7 +124,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     const int32_t *offs = step ? nullptr : a.offsets + (int64_t)b * (a.nb + 1);
     int n_pool, k_hi, kfull;
     if (step) {
-        n_pool = a.cache_lens[b];
+        n_pool = (a.lens_in_args && b < LENS_IN_ARGS) ? a.lens_arg[b] : a.cache_lens[b];
         k_hi = n_pool + a.Lq;
         kfull = k_hi;
     } else {
@@ -134,24 +136,6 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     const int ntile = (k_hi + KT - 1) / KT;
     const int t_begin = (int)((int64_t)split * ntile / a.nsplit);
     const int t_end = (int)((int64_t)(split + 1) * ntile / a.nsplit);
-
-    // ---- fused append: this work item's share of the new block -------------
-    // The G query heads of a group share one KV head, so only the items of
-    // its first head write; they split the new tokens evenly among them.
-    if (step && a.fuse_append && hh == 0) {
-        const int napp = a.nqt * a.nsplit;
-        const int ai = qi * a.nsplit + split;
-        const int s0 = (int)((int64_t)ai * a.Lq / napp);
-        const int s1 = (int)((int64_t)(ai + 1) * a.Lq / napp);
-        for (int u = tid; u < (s1 - s0) * CH; u += NT) {
-            const int t = s0 + u / CH, c = u % CH;
-            const int pos = n_pool + t;
-            const int page = a.page_table[(int64_t)b * a.max_pages + (pos >> 6)];
-            const int64_t dst = (((int64_t)page * a.Hkv + kvh) * KT + (pos & 63)) * D + 8 * c;
-            *(u32x4 *)(a.kpool + dst) = *(const u32x4 *)(a.kc + b * a.kc_sb + (int64_t)t * a.kc_st + kvh * a.kc_sh + 8 * c);
-            *(u32x4 *)(a.vpool + dst) = *(const u32x4 *)(a.vc + b * a.vc_sb + (int64_t)t * a.vc_st + kvh * a.vc_sh + 8 * c);
-        }
-    }
 
     // ---- this lane's query rows -----------------------------------------
     int rows[NB], kend[NB];
@@ -179,11 +163,58 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     }
 
     // ---- tile staging ---------------------------------------------------
-    // Physical page of a tile, read one tile ahead of its K/V loads so the
-    // dependent page-table load does not sit in front of them.
+    // Physical pages of the cache tiles: the first three are loaded at entry
+    // as independent loads (so the first K/V loads wait on one page-table
+    // read only); the rest of the split's page ids are staged in LDS before
+    // the first barrier, so no page-table read sits in front of a later tile.
+    const int32_t *ptab = a.page_table + (int64_t)b * a.max_pages;
+    const int tp_end = min(t_end, (n_pool + KT - 1) / KT);   // tiles with cache rows
+    auto page_glb = [&](int t) -> int { return t < tp_end ? ptab[t] : 0; };
+    const int pg0 = page_glb(t_begin), pg1 = page_glb(t_begin + 1), pg2 = page_glb(t_begin + 2);
+    const int n_lds_pages = min(max(tp_end - t_begin, 0), PAGE_LDS);
+    int pre[PAGE_LDS / NT];
+#pragma unroll
+    for (int k = 0; k < PAGE_LDS / NT; ++k) {
+        const int i = tid + k * NT;
+        pre[k] = i < n_lds_pages ? ptab[t_begin + i] : 0;
+    }
     auto page_of = [&](int t) -> int {
-        return (t < t_end && t * KT < n_pool) ? a.page_table[(int64_t)b * a.max_pages + t] : 0;
+        const int i = t - t_begin;
+        return i < PAGE_LDS ? page_lds[i] : page_glb(t);
     };
+
+    // Fused append, first round: this thread's chunk of the new block is
+    // loaded now and written after the prologue, off the critical path.  The
+    // G query heads of a group share one KV head, so only the items of its
+    // first head write; they split the new tokens evenly among them.
+    const bool appends = step && a.fuse_append && hh == 0;
+    int app_s0 = 0, app_n = 0;
+    if (appends) {
+        const int napp = a.nqt * a.nsplit;
+        const int ai = qi * a.nsplit + split;
+        app_s0 = (int)((int64_t)ai * a.Lq / napp);
+        app_n = ((int)((int64_t)(ai + 1) * a.Lq / napp) - app_s0) * CH;
+    }
+    auto app_src = [&](int u, int64_t &src_k, int64_t &src_v, int &pos, int &c) {
+        const int t = app_s0 + u / CH;
+        c = u % CH;
+        pos = n_pool + t;
+        src_k = b * a.kc_sb + (int64_t)t * a.kc_st + kvh * a.kc_sh + 8 * c;
+        src_v = b * a.vc_sb + (int64_t)t * a.vc_st + kvh * a.vc_sh + 8 * c;
+    };
+    auto app_dst = [&](int page, int pos, int c) -> int64_t {
+        return (((int64_t)page * a.Hkv + kvh) * KT + (pos & 63)) * D + 8 * c;
+    };
+    u32x4 app_k = {0, 0, 0, 0}, app_v = {0, 0, 0, 0};
+    int app_page = 0, app_pos = 0, app_c = 0;
+    const bool app_first = tid < app_n;
+    if (app_first) {
+        int64_t sk, sv;
+        app_src(tid, sk, sv, app_pos, app_c);
+        app_page = ptab[app_pos >> 6];
+        app_k = *(const u32x4 *)(a.kc + sk);
+        app_v = *(const u32x4 *)(a.vc + sv);
+    }
     // Per-thread parts of the K/V addresses, fixed for the whole loop: this
     // thread stages chunk c of rows row0 + i * (NT / CH) of every tile.
     constexpr int RSTEP = NT / CH;
@@ -194,11 +225,10 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     const uint16_t *vpool_t = a.vpool + ((int64_t)kvh * KT + row0) * D + 8 * cchunk;
     const uint16_t *kc_t = a.kc + b * a.kc_sb + kvh * a.kc_sh + 8 * cchunk;
     const uint16_t *vc_t = a.vc + b * a.vc_sb + kvh * a.vc_sh + 8 * cchunk;
-    u32x4 kreg[LOADS], vreg[LOADS];
-    int page_next = page_of(t_begin);
-    auto load_tile = [&](int kt) {
-        const int page = page_next;
-        page_next = page_of((kt >> 6) + 1);
+    // Two staging sets: the loads of tiles t+1 and t+2 are in flight while
+    // tile t is computed from LDS.
+    u32x4 kA[LOADS], vA[LOADS], kB[LOADS], vB[LOADS];
+    auto load_tile = [&](int kt, int page, u32x4 (&kreg)[LOADS], u32x4 (&vreg)[LOADS]) {
         if (kt + KT <= n_pool) {
             // whole tile in one cache page
             const int64_t po = (int64_t)page * page_elems;
@@ -232,7 +262,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
             }
         }
     };
-    auto store_tile = [&](int buf) {
+    auto store_tile = [&](int buf, const u32x4 (&kreg)[LOADS], const u32x4 (&vreg)[LOADS]) {
         char *ks = smem + buf * (KBYTES + VBYTES) + row0 * KP + 16 * cchunk;
         char *vs = smem + buf * (KBYTES + VBYTES) + KBYTES + row0 * VP + 16 * cchunk;
 #pragma unroll
@@ -244,18 +274,9 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
 
     const float c2 = a.scale_log2;
 
-    if (t_begin < t_end) {
-        load_tile(t_begin * KT);
-        store_tile(0);
-        __syncthreads();
-    }
-    for (int t = t_begin; t < t_end; ++t) {
-        const int buf = (t - t_begin) & 1;
-        const int kt = t * KT;
-        if (t + 1 < t_end) load_tile(kt + KT);
+    auto compute_tile = [&](int buf, int kt) {
         const char *ks = smem + buf * (KBYTES + VBYTES);
         const char *vs = ks + KBYTES;
-
         // S^T[key][query] = K Q^T for 64 keys x (32*NB) queries of this wave
         f32x16 s[2][NB];
 #pragma unroll
@@ -355,8 +376,51 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
             }
         }
 
-        if (t + 1 < t_end) store_tile(buf ^ 1);
+    };
+
+    // Pipeline: tile t is computed from LDS buffer (t - t_begin) & 1 while
+    // the loads of tiles t+1 and t+2 are in flight in the two register sets;
+    // after the compute, tile t+1 is stored to the other buffer and the loads
+    // of tile t+3 are issued.  One barrier per tile.  Unrolled by two so the
+    // register set of every step is fixed at compile time.
+    // Prologue: only the first tile is requested before the first compute,
+    // so it is not queued behind the next tiles of every other work-group;
+    // tiles 1 and 2 stream in while tile 0 is computed.
+    if (t_begin < t_end) {
+        load_tile(t_begin * KT, pg0, kA, vA);
+        store_tile(0, kA, vA);
+        if (t_begin + 1 < t_end) load_tile((t_begin + 1) * KT, pg1, kB, vB);
+        if (t_begin + 2 < t_end) load_tile((t_begin + 2) * KT, pg2, kA, vA);
+    }
+#pragma unroll
+    for (int k = 0; k < PAGE_LDS / NT; ++k)
+        if (tid + k * NT < n_lds_pages) page_lds[tid + k * NT] = pre[k];
+    if (app_first) {
+        const int64_t dst = app_dst(app_page, app_pos, app_c);
+        *(u32x4 *)(a.kpool + dst) = app_k;
+        *(u32x4 *)(a.vpool + dst) = app_v;
+    }
+    __syncthreads();
+    for (int t = t_begin; t < t_end; t += 2) {
+        compute_tile(0, t * KT);
+        if (t + 1 < t_end) store_tile(1, kB, vB);
+        if (t + 3 < t_end) load_tile((t + 3) * KT, page_of(t + 3), kB, vB);
         __syncthreads();
+        if (t + 1 >= t_end) break;
+        compute_tile(1, (t + 1) * KT);
+        if (t + 2 < t_end) store_tile(0, kA, vA);
+        if (t + 4 < t_end) load_tile((t + 4) * KT, page_of(t + 4), kA, vA);
+        __syncthreads();
+    }
+
+    // fused append, remaining rounds (more chunks than threads)
+    for (int u = tid + NT; u < app_n; u += NT) {
+        int64_t sk, sv;
+        int pos, c;
+        app_src(u, sk, sv, pos, c);
+        const int64_t dst = app_dst(ptab[pos >> 6], pos, c);
+        *(u32x4 *)(a.kpool + dst) = *(const u32x4 *)(a.kc + sk);
+        *(u32x4 *)(a.vpool + dst) = *(const u32x4 *)(a.vc + sv);
     }
 
     // ---- epilogue -------------------------------------------------------
@@ -393,8 +457,9 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
             if (a.lse && hf == 0)
                 a.lse[((int64_t)b * a.Hq + hq) * a.Lq + r] = (m[n] + __builtin_amdgcn_logf(lt)) * 0.69314718055994531f;
         } else {
-            const int64_t prow = (((int64_t)split * a.B + b) * a.Hq + hq) * a.Lq + r;
-            float *op = a.part_o + prow * D;
+            // register order: each store instruction writes 1 KB contiguous
+            const int64_t blk = (((int64_t)split * a.B + b) * a.Hq + hq) * a.nrb + (r >> 5);
+            float *op = a.part_o + blk * (32 * D) + 4 * lane;
 #pragma unroll
             for (int md = 0; md < MD; ++md)
 #pragma unroll
@@ -402,11 +467,11 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
                     f32x4 val;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) val[e] = o[n][md][4 * g + e];
-                    *(f32x4 *)(op + 32 * md + 8 * g + 4 * hf) = val;
+                    *(f32x4 *)(op + (md * 4 + g) * 256) = val;
                 }
             if (hf == 0) {
-                a.part_ml[2 * prow + 0] = m[n];
-                a.part_ml[2 * prow + 1] = lt;
+                a.part_ml[2 * (blk * 32 + l32) + 0] = m[n];
+                a.part_ml[2 * (blk * 32 + l32) + 1] = lt;
             }
         }
     }
@@ -415,53 +480,62 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
 // Merge the KV-split partials of every query row: with per-split running
 // max m_s (log2 domain), sum l_s and unnormalised o_s,
 //   M = max_s m_s,  L = sum_s l_s 2^(m_s - M),  o = sum_s o_s 2^(m_s - M) / L.
-// Splits are visited in a fixed order, so the result is deterministic.  One
-// thread owns 4 elements of a row; the split loops are unrolled so their
-// independent loads are in flight together.
+// Splits are visited in a fixed order, so the result is deterministic.  A
+// thread owns the 4 elements one accumulator lane holds for one (md, g), so
+// its partial reads are the writer's contiguous 1 KB runs; the split loops
+// are unrolled so their independent loads are in flight together.
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(const AttnArgs a) {
-    constexpr int TPR = D / 4;              // threads per row, 4 elements each
-    constexpr int RPB = 256 / TPR;          // rows per block
-    const int64_t nrows = (int64_t)a.B * a.Hq * a.Lq;
-    const int64_t row = (int64_t)blockIdx.x * RPB + threadIdx.x / TPR;
-    const int c4 = threadIdx.x % TPR;
-    if (row >= nrows) return;
-    const int r = (int)(row % a.Lq);
-    const int hq = (int)((row / a.Lq) % a.Hq);
-    const int b = (int)(row / ((int64_t)a.Lq * a.Hq));
+    constexpr int MD = D / 32;
+    constexpr int PER_BLK = MD * 4 * 64;      // float4 items per 32-row block
+    const int64_t nblk = (int64_t)a.B * a.Hq * a.nrb;
+    const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (u >= nblk * PER_BLK) return;
+    const int64_t blk = u / PER_BLK;
+    const int item = (int)(u % PER_BLK);
+    const int lane = item & 63;
+    const int mg = item >> 6;                 // md * 4 + g
+    const int r = (int)(blk % a.nrb) * 32 + (lane & 31);
+    if (r >= a.Lq) return;
+    const int hq = (int)((blk / a.nrb) % a.Hq);
+    const int b = (int)(blk / ((int64_t)a.nrb * a.Hq));
+    const int d0 = 32 * (mg >> 2) + 8 * (mg & 3) + 4 * (lane >> 5);
     const int S = a.nsplit;
-    const float2 *ml = (const float2 *)a.part_ml + row;
+    const float2 *ml = (const float2 *)a.part_ml + blk * 32 + (lane & 31);
+    const float *po = a.part_o + blk * (32 * D) + (int64_t)mg * 256 + 4 * lane;
+    const int64_t mls = nblk * 32;            // split stride of (m, l)
+    const int64_t ps = nblk * 32 * D;         // split stride of o
     float M = -INFINITY;
 #pragma unroll 8
-    for (int s = 0; s < S; ++s) M = fmaxf(M, ml[(int64_t)s * nrows].x);
+    for (int s = 0; s < S; ++s) M = fmaxf(M, ml[s * mls].x);
     const float Mu = (M == -INFINITY) ? 0.f : M;
     float L = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    const float *po = a.part_o + row * D + 4 * c4;
 #pragma unroll 8
     for (int s = 0; s < S; ++s) {
-        const float2 mls = ml[(int64_t)s * nrows];
-        const f32x4 ov = *(const f32x4 *)(po + (int64_t)s * nrows * D);
-        const float wgt = __builtin_amdgcn_exp2f(mls.x - Mu);
-        L += mls.y * wgt;
+        const float2 m_l = ml[s * mls];
+        const f32x4 ov = *(const f32x4 *)(po + s * ps);
+        const float wgt = __builtin_amdgcn_exp2f(m_l.x - Mu);
+        L += m_l.y * wgt;
 #pragma unroll
         for (int e = 0; e < 4; ++e) acc[e] += ov[e] * wgt;
     }
     const float inv = L > 0.f ? 1.f / L : 0.f;
     if (a.out_f32) {
-        float *op = (float *)a.out + b * a.o_sb + (int64_t)r * a.o_st + hq * a.o_sh + 4 * c4;
+        float *op = (float *)a.out + b * a.o_sb + (int64_t)r * a.o_st + hq * a.o_sh + d0;
         f32x4 val;
 #pragma unroll
         for (int e = 0; e < 4; ++e) val[e] = acc[e] * inv;
         *(f32x4 *)op = val;
     } else {
-        uint16_t *op = (uint16_t *)a.out + b * a.o_sb + (int64_t)r * a.o_st + hq * a.o_sh + 4 * c4;
+        uint16_t *op = (uint16_t *)a.out + b * a.o_sb + (int64_t)r * a.o_st + hq * a.o_sh + d0;
         u32x2 val;
         val[0] = pack_bf16x2(acc[0] * inv, acc[1] * inv);
         val[1] = pack_bf16x2(acc[2] * inv, acc[3] * inv);
         *(u32x2 *)op = val;
     }
-    if (a.lse && c4 == 0) a.lse[row] = (M + __builtin_amdgcn_logf(L)) * 0.69314718055994531f;
+    if (a.lse && mg == 0 && lane < 32)
+        a.lse[((int64_t)b * a.Hq + hq) * a.Lq + r] = (M + __builtin_amdgcn_logf(L)) * 0.69314718055994531f;
 }
 
 // Copy new tokens' K/V rows into their cache slots: one 16-byte chunk per
@@ -494,28 +568,25 @@ int launch_attn_t(const AttnArgs &a, hipStream_t st) {
 
 int launch_attention(const AttnArgs &a, int head_dim, TileShape shape, void *stream) {
     hipStream_t st = (hipStream_t)stream;
+    if (shape.nb != 1) return (int)hipErrorInvalidValue;
     if (head_dim == 128) {
-        if (shape.nb == 2 && shape.nw == 4) return launch_attn_t<128, 2, 4>(a, st);
-        if (shape.nb == 1 && shape.nw == 4) return launch_attn_t<128, 1, 4>(a, st);
-        if (shape.nb == 1 && shape.nw == 8) return launch_attn_t<128, 1, 8>(a, st);
+        if (shape.nw == 4) return launch_attn_t<128, 1, 4>(a, st);
+        if (shape.nw == 8) return launch_attn_t<128, 1, 8>(a, st);
     } else if (head_dim == 64) {
-        if (shape.nb == 2 && shape.nw == 4) return launch_attn_t<64, 2, 4>(a, st);
-        if (shape.nb == 1 && shape.nw == 4) return launch_attn_t<64, 1, 4>(a, st);
-        if (shape.nb == 1 && shape.nw == 8) return launch_attn_t<64, 1, 8>(a, st);
+        if (shape.nw == 4) return launch_attn_t<64, 1, 4>(a, st);
+        if (shape.nw == 8) return launch_attn_t<64, 1, 8>(a, st);
     }
     return (int)hipErrorInvalidValue;
 }
 
 int launch_combine(const AttnArgs &a, int head_dim, void *stream) {
     hipStream_t st = (hipStream_t)stream;
-    const int64_t nrows = (int64_t)a.B * a.Hq * a.Lq;
-    if (head_dim == 128) {
-        const int64_t grid = (nrows + 7) / 8;
+    const int64_t items = (int64_t)a.B * a.Hq * a.nrb * (head_dim / 32) * 4 * 64;
+    const int64_t grid = (items + 255) / 256;
+    if (head_dim == 128)
         hipLaunchKernelGGL(combine_kernel<128>, dim3((unsigned)grid), dim3(256), 0, st, a);
-    } else {
-        const int64_t grid = (nrows + 15) / 16;
+    else
         hipLaunchKernelGGL(combine_kernel<64>, dim3((unsigned)grid), dim3(256), 0, st, a);
-    }
     return (int)hipGetLastError();
 }
 
