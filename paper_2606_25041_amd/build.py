@@ -19,17 +19,35 @@ def hipcc():
     return os.path.join(rocm, "bin", "hipcc")
 
 
-def build(verbose=False):
-    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
-           "-Wall", "-Wno-unused-function",
-           # packed fp32 VALU ops stay off in every kernel
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           *SOURCES, "-o", LIB + ".tmp"]
+KERNEL_FLAGS = [
+    # packed fp32 VALU ops stay off in every kernel
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA results in VGPRs: the softmax reads every score with VALU
+    # instructions, which cannot address accumulation registers
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
+]
+
+
+def _run(cmd):
     res = subprocess.run(cmd, capture_output=True, text=True)
     msgs = [ln for ln in (res.stdout + res.stderr).splitlines()
-            if "packed-fp32-ops" not in ln]
+            if "packed-fp32-ops" not in ln and "--hip-link" not in ln]
     if res.returncode != 0:
-        raise RuntimeError("hipcc failed:\n" + "\n".join(msgs))
+        raise RuntimeError("hipcc failed:\n" + " ".join(cmd) + "\n" + "\n".join(msgs))
+    return msgs
+
+
+def build(verbose=False):
+    """Kernels (with their device code-generation flags) and the host-only
+    C ABI are compiled separately, then linked into one shared library."""
+    common = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
+              "-Wall", "-Wno-unused-function"]
+    kobj, aobj = LIB + ".kernels.o", LIB + ".api.o"
+    msgs = _run(common + KERNEL_FLAGS + ["-c", SOURCES[0], "-o", kobj])
+    msgs += _run(common + ["-c", SOURCES[1], "-o", aobj])
+    msgs += _run([hipcc(), f"--offload-arch={ARCH}", "-shared", kobj, aobj, "-o", LIB + ".tmp"])
+    for f in (kobj, aobj):
+        os.remove(f)
     if verbose and msgs:
         print("\n".join(msgs))
     os.replace(LIB + ".tmp", LIB)

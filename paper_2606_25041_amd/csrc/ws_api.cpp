@@ -41,6 +41,10 @@ int env_int(const char *name, int dflt) {
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
+// Token stride limit of key/value tensors (elements): the kernels form the
+// offsets of one 64-key tile's rows in 32 bits.
+constexpr int64_t WS_MAX_KV_TOKEN_STRIDE = (int64_t)1 << 24;
+
 // Checks pointer, dtype, alignment and strides of one token tensor.
 int check_tensor(const char *name, const ws_tensor4 &t, bool allow_f32) {
     if (!t.ptr) return fail(WS_ERR_NULL, "%s.ptr is NULL", name);
@@ -51,6 +55,14 @@ int check_tensor(const char *name, const ws_tensor4 &t, bool allow_f32) {
     const int64_t q = (t.dtype == WS_DTYPE_BF16) ? 8 : 4;  // elements per 16 bytes
     if (!aligned16(t.ptr) || t.stride_b % q || t.stride_t % q || t.stride_h % q)
         return fail(WS_ERR_ALIGN, "%s: pointer must be 16-byte aligned and strides multiples of 16 bytes", name);
+    return WS_OK;
+}
+
+int check_kv_tensor(const char *name, const ws_tensor4 &t) {
+    if (int rc = check_tensor(name, t, false)) return rc;
+    if (t.stride_t >= WS_MAX_KV_TOKEN_STRIDE)
+        return fail(WS_ERR_SHAPE, "%s token stride %lld must be below %lld elements", name,
+                    (long long)t.stride_t, (long long)WS_MAX_KV_TOKEN_STRIDE);
     return WS_OK;
 }
 
@@ -97,21 +109,12 @@ struct StepPlan {
 // Query tile and KV split count of a streaming step.  Splits are added only
 // while the work-groups still fit one round on the CUs, and every split
 // keeps at least two 64-key tiles.
-// Tuning override: WS_SHAPE=<32-query blocks per wave><waves per group>,
-// "14" or "18".
-bool shape_override(ws::TileShape &s) {
-    const int v = env_int("WS_SHAPE", 0);
-    const ws::TileShape c{v / 10, v % 10};
-    if (c.nb == 1 && (c.nw == 4 || c.nw == 8)) {
-        s = c;
-        return true;
-    }
-    return false;
-}
+// One launch shape: 8 waves x 32 query rows (256-query tiles).
+ws::TileShape default_shape() { return ws::TileShape{1, 8}; }
 
 StepPlan plan_step(int batch, int hq, int lq, int64_t max_k) {
     StepPlan p;
-    if (!shape_override(p.shape)) p.shape = (lq > 128) ? ws::TileShape{1, 8} : ws::TileShape{1, 4};
+    p.shape = default_shape();
     const int qt = p.shape.qtile();
     p.nqt = (lq + qt - 1) / qt;
     const int64_t base = (int64_t)batch * hq * p.nqt;
@@ -136,11 +139,7 @@ size_t step_workspace(const StepPlan &p, int batch, int hq, int lq) {
     return (size_t)p.nsplit * batch * hq * rows * (WS_MAX_HEAD_DIM + 2) * sizeof(float);
 }
 
-ws::TileShape plan_prefill(int seq_len) {
-    ws::TileShape s;
-    if (shape_override(s)) return s;
-    return seq_len > 128 ? ws::TileShape{1, 8} : ws::TileShape{1, 4};
-}
+ws::TileShape plan_prefill(int) { return default_shape(); }
 
 // Total work items; fails when the grid would not fit the kernel's int math.
 bool finish_work(ws::AttnArgs &a) {
@@ -222,8 +221,8 @@ int ws_block_causal_attn_fwd(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, c
         return fail(WS_ERR_SHAPE, "batch %d, new_len %d, num_q_heads %d", (int)batch, (int)new_len, (int)num_q_heads);
     if (batch == 0 || new_len == 0) return ok();  // no query row: nothing is read or written
     if (int rc = check_tensor("q", q, false)) return rc;
-    if (int rc = check_tensor("k_new", k_new, false)) return rc;
-    if (int rc = check_tensor("v_new", v_new, false)) return rc;
+    if (int rc = check_kv_tensor("k_new", k_new)) return rc;
+    if (int rc = check_kv_tensor("v_new", v_new)) return rc;
     if (int rc = check_tensor("out", out, true)) return rc;
     if (flags & ~WS_FUSE_APPEND) return fail(WS_ERR_UNSUPPORTED, "unknown flags 0x%x", (unsigned)flags);
     if (!(scale > 0.f) || !std::isfinite(scale)) return fail(WS_ERR_UNSUPPORTED, "scale must be finite and > 0");
@@ -294,8 +293,8 @@ int ws_block_causal_prefill(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, const ws_p
         if (!kv_or_null) return fail(WS_ERR_NULL, "k/v are NULL and no paged cache was given");
         if (int rc = check_paged(kv_or_null)) return rc;
     } else {
-        if (int rc = check_tensor("k", k, false)) return rc;
-        if (int rc = check_tensor("v", v, false)) return rc;
+        if (int rc = check_kv_tensor("k", k)) return rc;
+        if (int rc = check_kv_tensor("v", v)) return rc;
     }
     if (int rc = check_tensor("q", q, false)) return rc;
     if (int rc = check_tensor("out", out, true)) return rc;

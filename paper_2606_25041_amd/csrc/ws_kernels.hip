@@ -8,22 +8,25 @@
 // (Sec. 2.4).
 //
 // Attention kernel design (one work-group = one (stream, query head,
-// query tile, KV split) work item; waves own 32*NB query rows each):
+// query tile, KV split) work item; 8 waves x 32 query rows = 256 rows):
 //  * S^T = K Q^T on v_mfma_f32_32x32x16_bf16: K (A operand) from LDS, Q (B
 //    operand) resident in registers.  In the 32x32 accumulator layout a lane
 //    owns one query column and 16 keys, so row max/sum are in-lane plus one
 //    v_permlane32_swap per 64-key tile.
 //  * Online softmax in the log2 domain (scale*log2(e) folded into one FMA),
-//    fp32 running max/sum per lane.
+//    fp32 running max/sum per lane, lazy rescale of O.
 //  * O^T += V^T P^T on the same MFMA: P stays in registers (the accumulator
 //    layout of S^T is exactly the B-operand layout once the 16 keys of each
 //    MFMA step are permuted consistently on both operands); V is read with
 //    ds_read_b64_tr_b16 from a row-major LDS tile, so no transpose pass.
-//    Each lane owns one query column of O^T, so the softmax rescale is a
-//    per-lane scalar multiply.
-//  * K/V tiles of 64 keys (= one cache page) are staged global -> VGPR ->
-//    LDS with 128-bit loads, double-buffered in LDS (one barrier per tile),
-//    the next tile's loads in flight during the current tile's MFMAs.
+//  * K/V tiles of 64 keys (= one cache page) go from global memory straight
+//    into a 4-stage LDS ring (global_load_lds_dwordx4), two tiles in flight
+//    while the current one is used; rows are XOR-swizzled in 16-byte chunks
+//    so both the K reads and the V transpose reads are bank-conflict free.
+//  * Two waves share each SIMD and run the same loop one block apart: while
+//    one issues the MFMAs of a tile (P V of the previous tile, S^T of this
+//    one), the other computes its softmax; a work-group barrier separates
+//    the blocks.
 //  * Tiles past the last visible key of the query tile are never loaded
 //    (block-granularity skip); tiles fully visible to every row of the query
 //    tile run without element masks; only the tiles straddling a block
@@ -50,6 +53,7 @@ constexpr int KT = 64;        // keys per tile (= page size)
 constexpr int NUM_XCD = 8;    // MI355X: 8 XCDs, work-groups dispatched round-robin
 constexpr float RESCALE_LOG2 = 8.f;  // lazy-rescale threshold (log2 units)
 constexpr int PAGE_LDS = 2560;       // page ids of a split staged in LDS (more: read from memory)
+constexpr int NSTAGE = 4;            // K/V tiles resident in the LDS ring
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
@@ -65,14 +69,23 @@ __device__ __forceinline__ float halves_sum(float x) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Read-only metadata (page tables, cache lengths, block offsets) read at a
+// wave-uniform index goes through the constant address space, so it becomes a
+// scalar load: it does not count against the vector-memory counter that the
+// tile pipeline waits on.
+typedef const __attribute__((address_space(4))) int32_t cint32;
+__device__ __forceinline__ int ld_uniform(const int32_t *p, int64_t i) { return ((const cint32 *)p)[i]; }
+
 // End (exclusive) of the block that holds token i: the first offset > i.
+template <bool UNIFORM>
 __device__ __forceinline__ int block_end(const int32_t *off, int nb, int i) {
+    auto at = [&](int k) { return UNIFORM ? ld_uniform(off, k) : off[k]; };
     int lo = 1, hi = nb;  // answer index in [1, nb]
     while (lo < hi) {
         int mid = (lo + hi) >> 1;
-        if (off[mid] > i) hi = mid; else lo = mid + 1;
+        if (at(mid) > i) hi = mid; else lo = mid + 1;
     }
-    return off[lo];
+    return at(lo);
 }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -80,20 +93,61 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
 }
 
-template <int D, int NB, int NW>
+// s_waitcnt with vector-memory count <= N and LDS/scalar count = 0 (the export
+// count is not waited on).  gfx9 encoding: vmcnt[3:0], expcnt[6:4],
+// lgkmcnt[11:8], vmcnt[5:4] in bits [15:14].
+template <int N>
+__device__ __forceinline__ void wait_vm_lgkm() {
+    static_assert(N >= 0 && N < 64, "vmcnt has 6 bits");
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
+}
+
+// Work-group barrier without the memory fence of __syncthreads(): that fence
+// also waits for every direct-to-LDS load in flight, and the pipeline keeps
+// two tiles in flight across each barrier.  The explicit waits in front of
+// each barrier make the LDS data it publishes complete.
+__device__ __forceinline__ void wg_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// LDS layout of a key tile: rows of D bf16, no padding; 16-byte chunk c of
+// key row r sits in slot c ^ swz(r) of that row.  With this swizzle the K
+// reads of S^T (16 consecutive rows, one chunk) and the V transpose reads of
+// O^T (4 rows x 4 chunks per 32 lanes) each touch 16 distinct 16-byte bank
+// groups.
+template <int D>
+__device__ __forceinline__ int swz(int r) {
+    if constexpr (D == 128) return 4 * (r & 3) + ((r >> 2) & 3);   // 256-byte rows
+    else return 4 * ((r >> 1) & 1) + ((r >> 2) & 3);                // 128-byte rows, two per bank line
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+
+// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane;
+// lds must be the same for the whole wave.
+__device__ __forceinline__ void dma16(const void *g, char *lds) {
+    __builtin_amdgcn_global_load_lds(g, (lds_void *)lds, 16, 0, 0);
+}
+
+template <int D, int NW, int NB>
 __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     constexpr int NT = NW * 64;
-    constexpr int QT = NW * 32 * NB;
-    constexpr int CH = D / 8;             // 16-byte chunks per key row
-    constexpr int KP = D * 2 + 16;        // K row pitch in LDS (bytes): conflict-free b128 reads
-    constexpr int VP = D * 2 + 32;        // V row pitch in LDS (bytes): conflict-free transpose reads
-    constexpr int KBYTES = KT * KP;
-    constexpr int VBYTES = KT * VP;
-    constexpr int LOADS = KT * CH / NT;   // 16-byte chunks per thread per tile, each of K and V
-    constexpr int KK = D / 16;            // MFMA k-steps over head_dim for S
-    constexpr int MD = D / 32;            // 32-row blocks of head_dim for O^T
-    static_assert((KT * CH) % NT == 0, "tile chunks must divide among threads");
-    __shared__ __attribute__((aligned(16))) char smem[2 * (KBYTES + VBYTES)];
+    constexpr int QT = NW * 32 * NB;       // query rows per work-group
+    constexpr int ROWB = 2 * D;            // bytes of one key row
+    constexpr int TILEB = KT * ROWB;       // bytes of one K (or V) tile
+    constexpr int RPW = 1024 / ROWB;       // key rows per wave-wide 16-byte load
+    constexpr int LPR = ROWB / 16;         // lanes per key row in such a load
+    constexpr int NWD = NW / 2;            // waves that load tiles (the leading half)
+    constexpr int NI = TILEB / (NWD * 1024);  // wave-wide loads per loading wave per tile, each of K and V
+    constexpr int KK = D / 16;             // MFMA k-steps over head_dim for S^T
+    constexpr int MD = D / 32;             // 32-row blocks of head_dim for O^T
+    constexpr int VRING = NSTAGE * TILEB;  // byte offset of the V ring
+    static_assert(NI >= 1 && TILEB % (NWD * 1024) == 0, "a tile splits into wave-wide loads");
+    __shared__ __attribute__((aligned(1024))) char smem[2 * NSTAGE * TILEB];
     __shared__ int page_lds[PAGE_LDS];
 
     // ---- work item ------------------------------------------------------
@@ -116,7 +170,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int hf = lane >> 5;     // which half of the wave
     const int l32 = lane & 31;
 
@@ -124,32 +178,148 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     const int32_t *offs = step ? nullptr : a.offsets + (int64_t)b * (a.nb + 1);
     int n_pool, k_hi, kfull;
     if (step) {
-        n_pool = (a.lens_in_args && b < LENS_IN_ARGS) ? a.lens_arg[b] : a.cache_lens[b];
+        n_pool = (a.lens_in_args && b < LENS_IN_ARGS) ? a.lens_arg[b] : ld_uniform(a.cache_lens, b);
         k_hi = n_pool + a.Lq;
         kfull = k_hi;
     } else {
         n_pool = a.paged ? a.Lq : 0;
         const int q_last = min(q0 + QT, a.Lq) - 1;
-        k_hi = block_end(offs, a.nb, q_last);
-        kfull = block_end(offs, a.nb, q0);
+        k_hi = block_end<true>(offs, a.nb, q_last);
+        kfull = block_end<true>(offs, a.nb, q0);
     }
     const int ntile = (k_hi + KT - 1) / KT;
     const int t_begin = (int)((int64_t)split * ntile / a.nsplit);
     const int t_end = (int)((int64_t)(split + 1) * ntile / a.nsplit);
 
-    // ---- this lane's query rows -----------------------------------------
-    int rows[NB], kend[NB];
+    // ---- page ids -------------------------------------------------------
+    // The first three tiles' pages are read up front; the rest of the
+    // split's page ids are staged in LDS once, so no page-table read sits in
+    // front of a later tile's loads.
+    const int32_t *ptab = a.page_table + (int64_t)b * a.max_pages;
+    const int tp_end = min(t_end, (n_pool + KT - 1) / KT);   // tiles with cache rows
+    auto page_glb = [&](int t) -> int { return t < tp_end ? ld_uniform(ptab, t) : 0; };
+    const int n_lds_pages = min(max(tp_end - t_begin, 0), PAGE_LDS);
+    int pre[PAGE_LDS / NT];
+#pragma unroll
+    for (int k = 0; k < PAGE_LDS / NT; ++k) {
+        const int i = tid + k * NT;
+        pre[k] = i < n_lds_pages ? ptab[t_begin + i] : 0;
+    }
+    auto page_of = [&](int t) -> int {
+        const int i = t - t_begin;
+        return i < PAGE_LDS ? __builtin_amdgcn_readfirstlane(page_lds[i]) : page_glb(t);
+    };
+    const int pg0 = page_glb(t_begin), pg1 = page_glb(t_begin + 1), pg2 = page_glb(t_begin + 2);
+
+    // ---- this lane's query rows -------------------------------------------
+    // row n of the lane: q0 + wave * 32 * NB + 32 * n + l32
+    int row[NB], kend[NB];
     bf16x8 qf[NB][KK];
 #pragma unroll
     for (int n = 0; n < NB; ++n) {
-        rows[n] = q0 + wave * 32 * NB + n * 32 + l32;
-        const int rc = min(rows[n], a.Lq - 1);
-        kend[n] = step ? k_hi : block_end(offs, a.nb, rc);
+        row[n] = q0 + wave * 32 * NB + 32 * n + l32;
+        const int rc = min(row[n], a.Lq - 1);
+        kend[n] = step ? k_hi : block_end<false>(offs, a.nb, rc);
         const uint16_t *qp = a.q + b * a.q_sb + (int64_t)rc * a.q_st + hq * a.q_sh + 8 * hf;
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) qf[n][kk] = *(const bf16x8 *)(qp + 16 * kk);
     }
 
+    // ---- direct-to-LDS tile loads -----------------------------------------
+    // The leading waves (wave < NWD) load the tiles.  Wave-wide load i of
+    // such a wave fills tile bytes [(i * NWD + wave) * 1024, +1024): lane
+    // `lane` writes 16 bytes at +16 * lane, i.e. slot lane % LPR of key row
+    // lrow0 + i * NWD * RPW, and so fetches the chunk that belongs there,
+    // lch = slot ^ swz(row).  The swizzle depends on the row modulo 16 only,
+    // so lch is the same for all i.
+    static_assert((NWD * RPW) % 16 == 0, "the swizzle must repeat across a wave's loads");
+    const int lrow0 = wave * RPW + lane / LPR;
+    const int lch = (lane % LPR) ^ swz<D>(lrow0);
+    const char *kpool_b = (const char *)a.kpool;
+    const char *vpool_b = (const char *)a.vpool;
+    const char *kc_b = (const char *)(a.kc + b * a.kc_sb + kvh * a.kc_sh);
+    const char *vc_b = (const char *)(a.vc + b * a.vc_sb + kvh * a.vc_sh);
+    const int64_t kst2 = 2 * a.kc_st, vst2 = 2 * a.vc_st;
+    // per-lane byte offsets: within a (page, KV head) tile, and within the
+    // contiguous rows starting at this wave's first row (token strides are
+    // below 2^24 elements, checked on the host)
+    uint32_t lofs_p = (uint32_t)(lrow0 * ROWB + 16 * lch);
+    uint32_t lofs_k = (uint32_t)((lane / LPR) * kst2 + 16 * lch);
+    uint32_t lofs_v = (uint32_t)((lane / LPR) * vst2 + 16 * lch);
+    // issue the loads of tile u (its physical page, if cached, is `page`,
+    // wave-uniform) into ring stage s: NI wave-wide loads for K and for V
+    auto issue_tile = [&](int u, int s, int page) {
+        const int kt = u * KT;
+        char *kd = smem + s * TILEB + wave * 1024;
+        char *vd = smem + VRING + s * TILEB + wave * 1024;
+        const int64_t tb = ((int64_t)page * a.Hkv + kvh) * TILEB;
+        const char *kg = kpool_b + tb, *vg = vpool_b + tb;
+        if (kt + KT <= n_pool) {
+            // whole tile in one cache page
+#pragma unroll
+            for (int i = 0; i < NI; ++i) {
+                dma16(kg + i * NWD * 1024 + lofs_p, kd + i * NWD * 1024);
+                dma16(vg + i * NWD * 1024 + lofs_p, vd + i * NWD * 1024);
+            }
+        } else if (kt >= n_pool && kt + KT <= k_hi) {
+            // whole tile in the contiguous keys
+            const int64_t j0 = kt - n_pool + wave * RPW;
+#pragma unroll
+            for (int i = 0; i < NI; ++i) {
+                const int64_t j = j0 + i * NWD * RPW;
+                dma16(kc_b + j * kst2 + lofs_k, kd + i * NWD * 1024);
+                dma16(vc_b + j * vst2 + lofs_v, vd + i * NWD * 1024);
+            }
+        } else {
+            // the tile straddles the cache end or runs past the last key:
+            // rows past the end repeat the last key (their scores are masked)
+            const int64_t c0 = (int64_t)(kt - n_pool);   // contiguous row of the tile's first key
+            const char *kcg = kc_b + c0 * kst2, *vcg = vc_b + c0 * vst2;
+            const uint32_t lofs_c = lofs_p - lrow0 * ROWB;   // the chunk's byte offset in a row
+#pragma unroll
+            for (int i = 0; i < NI; ++i) {
+                const int r = min(lrow0 + i * NWD * RPW, k_hi - 1 - kt);   // row within the tile
+                const char *gk, *gv;
+                if (kt + r < n_pool) {
+                    gk = kg + (uint32_t)(r * ROWB) + lofs_c;
+                    gv = vg + (uint32_t)(r * ROWB) + lofs_c;
+                } else {
+                    gk = kcg + (uint32_t)(r * kst2) + lofs_c;
+                    gv = vcg + (uint32_t)(r * vst2) + lofs_c;
+                }
+                dma16(gk, kd + i * NWD * 1024);
+                dma16(gv, vd + i * NWD * 1024);
+            }
+        }
+        // the waits count this tile's loads as one group: keep later memory
+        // operations from being moved in between
+        asm volatile("" ::: "memory");
+    };
+    // wait until at most `younger` tiles' loads are still in flight
+    auto wait_tiles = [&](int younger) {
+        if (younger >= 2) wait_vm_lgkm<4 * NI>();
+        else if (younger == 1) wait_vm_lgkm<2 * NI>();
+        else wait_vm_lgkm<0>();
+    };
+
+    // ---- LDS read addresses -----------------------------------------------
+    // K (A operand of S^T = K Q^T): lane (l32, hf) reads key row 32 * mb + l32,
+    // chunk 2 * kk + hf, at kbase ^ (32 * kk): the row offset has no bits
+    // below 128 and chunk 2 * kk ^ swz only changes bits 5.. of the slot.
+    uint32_t kbase = l32 * ROWB + 16 * (hf ^ swz<D>(l32));
+    // V^T fragments (A operand of O^T += V^T P^T) by transpose reads: lane
+    // reads key rows 16 * ks4 + vr and +8, 4 head-dim columns of chunk
+    // 4 * md + vc, at vbase[e] ^ (64 * md).
+    const int j16 = lane & 15;
+    uint32_t vbase[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+        const int vr = 4 * hf + (j16 >> 2) + 8 * e;
+        const int vc = 2 * ((lane >> 4) & 1) + ((j16 & 3) >> 1);
+        vbase[e] = VRING + vr * ROWB + 16 * (vc ^ swz<D>(vr)) + 8 * (j16 & 1);
+    }
+
+    const float c2 = a.scale_log2;
     f32x16 o[NB][MD];
     float m[NB], l[NB];
 #pragma unroll
@@ -162,168 +332,80 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
             for (int v = 0; v < 16; ++v) o[n][md][v] = 0.f;
     }
 
-    // ---- tile staging ---------------------------------------------------
-    // Physical pages of the cache tiles: the first three are loaded at entry
-    // as independent loads (so the first K/V loads wait on one page-table
-    // read only); the rest of the split's page ids are staged in LDS before
-    // the first barrier, so no page-table read sits in front of a later tile.
-    const int32_t *ptab = a.page_table + (int64_t)b * a.max_pages;
-    const int tp_end = min(t_end, (n_pool + KT - 1) / KT);   // tiles with cache rows
-    auto page_glb = [&](int t) -> int { return t < tp_end ? ptab[t] : 0; };
-    const int pg0 = page_glb(t_begin), pg1 = page_glb(t_begin + 1), pg2 = page_glb(t_begin + 2);
-    const int n_lds_pages = min(max(tp_end - t_begin, 0), PAGE_LDS);
-    int pre[PAGE_LDS / NT];
-#pragma unroll
-    for (int k = 0; k < PAGE_LDS / NT; ++k) {
-        const int i = tid + k * NT;
-        pre[k] = i < n_lds_pages ? ptab[t_begin + i] : 0;
-    }
-    auto page_of = [&](int t) -> int {
-        const int i = t - t_begin;
-        return i < PAGE_LDS ? page_lds[i] : page_glb(t);
-    };
+    constexpr int NQK = 2 * KK;       // K fragments (steps) of S^T per tile; NB MFMAs each
+    constexpr int NPV = 4 * MD;       // V fragments (steps) of O^T per tile; NB MFMAs each
+    constexpr int SPQ = 32 * NB / NQK;   // softmax scores per S^T step
+    constexpr int SPV = 32 * NB / NPV;   // scores per O^T step folded into the next row max
+    static_assert(SPQ % 2 == 0 && SPV % 2 == 0, "scores go in pairs");
+    typedef f32x16 Tile[NB][2];      // S^T of one tile: per query block, two 32-key blocks
 
-    // Fused append, first round: this thread's chunk of the new block is
-    // loaded now and written after the prologue, off the critical path.  The
-    // G query heads of a group share one KV head, so only the items of its
-    // first head write; they split the new tokens evenly among them.
-    const bool appends = step && a.fuse_append && hh == 0;
-    int app_s0 = 0, app_n = 0;
-    if (appends) {
-        const int napp = a.nqt * a.nsplit;
-        const int ai = qi * a.nsplit + split;
-        app_s0 = (int)((int64_t)ai * a.Lq / napp);
-        app_n = ((int)((int64_t)(ai + 1) * a.Lq / napp) - app_s0) * CH;
-    }
-    auto app_src = [&](int u, int64_t &src_k, int64_t &src_v, int &pos, int &c) {
-        const int t = app_s0 + u / CH;
-        c = u % CH;
-        pos = n_pool + t;
-        src_k = b * a.kc_sb + (int64_t)t * a.kc_st + kvh * a.kc_sh + 8 * c;
-        src_v = b * a.vc_sb + (int64_t)t * a.vc_st + kvh * a.vc_sh + 8 * c;
+    // (soff: byte offset of a ring stage, a multiple of TILEB, so adding it
+    // commutes with the XORs on the low address bits)
+    // K fragment of S^T step i (kk = i / 2, key block mb = i % 2)
+    auto kread = [&](uint32_t kb, int i) -> bf16x8 {
+        return *(const bf16x8 *)(smem + (i & 1) * 32 * ROWB + (kb ^ (32 * (i >> 1))));
     };
-    auto app_dst = [&](int page, int pos, int c) -> int64_t {
-        return (((int64_t)page * a.Hkv + kvh) * KT + (pos & 63)) * D + 8 * c;
+    // V^T fragment of O^T step i (ks4 = i / MD, md = i % MD) by two
+    // transpose reads
+    auto vread = [&](uint32_t v0, uint32_t v1, int i) -> bf16x8 {
+        const int ks4 = i / MD, md = i % MD;
+        const i16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_i16x4 *)(smem + ks4 * 16 * ROWB + (v0 ^ (64 * md))));
+        const i16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_i16x4 *)(smem + ks4 * 16 * ROWB + (v1 ^ (64 * md))));
+        // whole-vector reinterpretation: element-wise bf16 casts of the
+        // transpose-read result were lowered to a splat
+        return __builtin_bit_cast(bf16x8, __builtin_shufflevector(va, vb, 0, 1, 2, 3, 4, 5, 6, 7));
     };
-    u32x4 app_k = {0, 0, 0, 0}, app_v = {0, 0, 0, 0};
-    int app_page = 0, app_pos = 0, app_c = 0;
-    const bool app_first = tid < app_n;
-    if (app_first) {
-        int64_t sk, sv;
-        app_src(tid, sk, sv, app_pos, app_c);
-        app_page = ptab[app_pos >> 6];
-        app_k = *(const u32x4 *)(a.kc + sk);
-        app_v = *(const u32x4 *)(a.vc + sv);
-    }
-    // Per-thread parts of the K/V addresses, fixed for the whole loop: this
-    // thread stages chunk c of rows row0 + i * (NT / CH) of every tile.
-    constexpr int RSTEP = NT / CH;
-    const int row0 = tid / CH;
-    const int cchunk = tid % CH;
-    const int64_t page_elems = (int64_t)a.Hkv * KT * D;
-    const uint16_t *kpool_t = a.kpool + ((int64_t)kvh * KT + row0) * D + 8 * cchunk;
-    const uint16_t *vpool_t = a.vpool + ((int64_t)kvh * KT + row0) * D + 8 * cchunk;
-    const uint16_t *kc_t = a.kc + b * a.kc_sb + kvh * a.kc_sh + 8 * cchunk;
-    const uint16_t *vc_t = a.vc + b * a.vc_sb + kvh * a.vc_sh + 8 * cchunk;
-    // Two staging sets: the loads of tiles t+1 and t+2 are in flight while
-    // tile t is computed from LDS.
-    u32x4 kA[LOADS], vA[LOADS], kB[LOADS], vB[LOADS];
-    auto load_tile = [&](int kt, int page, u32x4 (&kreg)[LOADS], u32x4 (&vreg)[LOADS]) {
-        if (kt + KT <= n_pool) {
-            // whole tile in one cache page
-            const int64_t po = (int64_t)page * page_elems;
+    // score e (0..32*NB-1) of a tile: query block n = e / 32, and within it
+    // in P's B-operand order (fragment ks4 = e % 32 / 8 holds keys
+    // 8 * (ks4 & 1) + e % 8 of key block ks4 / 2)
+    auto score = [&](const Tile &sc, int e) -> float { return sc[e >> 5][(e >> 4) & 1][e & 15]; };
+    // P weights of scores e and e+1: 2^(s * c2 - m), rounded to bf16 for
+    // P.V; l accumulates them in fp32 (so lse is exact to fp32 rounding)
+    auto softmax_pair = [&](const Tile &sc, bf16x8 (&pf)[NB][4], int e, const float (&m_use)[NB],
+                            float &lacc) {
+        const int n = e >> 5, f = e & 31;
+        const float x0 = fast_exp2(__builtin_fmaf(score(sc, e), c2, -m_use[n]));
+        const float x1 = fast_exp2(__builtin_fmaf(score(sc, e + 1), c2, -m_use[n]));
+        pf[n][f >> 3][f & 7] = (__bf16)x0;
+        pf[n][f >> 3][(f & 7) + 1] = (__bf16)x1;
+        lacc += x0;
+        lacc += x1;
+        asm volatile("" : "+v"(lacc));   // keep the sum beside its exps
+    };
+    // in-lane max of a tile's scores per query block; the other half-wave's
+    // keys are folded in by update_max
+    auto lane_max = [&](const Tile &sc, float (&mx)[NB]) {
 #pragma unroll
-            for (int i = 0; i < LOADS; ++i) {
-                kreg[i] = *(const u32x4 *)(kpool_t + po + i * RSTEP * D);
-                vreg[i] = *(const u32x4 *)(vpool_t + po + i * RSTEP * D);
-            }
-        } else if (kt >= n_pool && kt + KT <= k_hi) {
-            // whole tile in the contiguous keys
-            const int64_t j0 = kt - n_pool + row0;
+        for (int n = 0; n < NB; ++n) {
+            mx[n] = -INFINITY;
 #pragma unroll
-            for (int i = 0; i < LOADS; ++i) {
-                kreg[i] = *(const u32x4 *)(kc_t + (j0 + i * RSTEP) * a.kc_st);
-                vreg[i] = *(const u32x4 *)(vc_t + (j0 + i * RSTEP) * a.vc_st);
-            }
-        } else {
-            // the tile straddles the cache end or runs past the last key:
-            // rows past the end repeat a valid row (their scores are masked)
-#pragma unroll
-            for (int i = 0; i < LOADS; ++i) {
-                const int j = min(kt + row0 + i * RSTEP, k_hi - 1);
-                if (j < n_pool) {
-                    const int64_t po = (int64_t)page * page_elems + (int64_t)((j & 63) - row0) * D;
-                    kreg[i] = *(const u32x4 *)(kpool_t + po);
-                    vreg[i] = *(const u32x4 *)(vpool_t + po);
-                } else {
-                    kreg[i] = *(const u32x4 *)(kc_t + (int64_t)(j - n_pool) * a.kc_st);
-                    vreg[i] = *(const u32x4 *)(vc_t + (int64_t)(j - n_pool) * a.vc_st);
-                }
-            }
+            for (int e = 0; e < 32; ++e) mx[n] = fmaxf(mx[n], score(sc, 32 * n + e));
         }
     };
-    auto store_tile = [&](int buf, const u32x4 (&kreg)[LOADS], const u32x4 (&vreg)[LOADS]) {
-        char *ks = smem + buf * (KBYTES + VBYTES) + row0 * KP + 16 * cchunk;
-        char *vs = smem + buf * (KBYTES + VBYTES) + KBYTES + row0 * VP + 16 * cchunk;
+    // element masks only where the tile is not visible to every row
+    auto mask = [&](int t, Tile &sc) {
+        const int kt = t * KT;
 #pragma unroll
-        for (int i = 0; i < LOADS; ++i) {
-            *(u32x4 *)(ks + i * RSTEP * KP) = kreg[i];
-            *(u32x4 *)(vs + i * RSTEP * VP) = vreg[i];
-        }
-    };
-
-    const float c2 = a.scale_log2;
-
-    auto compute_tile = [&](int buf, int kt) {
-        const char *ks = smem + buf * (KBYTES + VBYTES);
-        const char *vs = ks + KBYTES;
-        // S^T[key][query] = K Q^T for 64 keys x (32*NB) queries of this wave
-        f32x16 s[2][NB];
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-            for (int n = 0; n < NB; ++n)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) s[mb][n][v] = 0.f;
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-#pragma unroll
-            for (int mb = 0; mb < 2; ++mb) {
-                const bf16x8 ka = *(const bf16x8 *)(ks + (mb * 32 + l32) * KP + (16 * kk + 8 * hf) * 2);
-#pragma unroll
-                for (int n = 0; n < NB; ++n)
-                    s[mb][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[n][kk], s[mb][n], 0, 0, 0);
-            }
-        }
-
-        // element masks only where the tile is not visible to every row
-        if (kt + KT > kfull) {
+        for (int n = 0; n < NB; ++n)
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
                     const int key = kt + mb * 32 + (v >> 2) * 8 + 4 * hf + (v & 3);
-#pragma unroll
-                    for (int n = 0; n < NB; ++n)
-                        if (key >= kend[n]) s[mb][n][v] = -INFINITY;
+                    if (key >= kend[n]) sc[n][mb][v] = -INFINITY;
                 }
-        }
-
-        // online softmax (log2 domain)
-        bf16x8 pf[NB][4];
+    };
+    // Running max (log2 domain) from a tile's in-lane max, with lazy rescale:
+    // m only moves when the tile max exceeds it by more than 2^RESCALE_LOG2,
+    // so most tiles skip rescaling O and l (a wave-uniform branch).  Weights
+    // stay <= 2^RESCALE_LOG2; O and l share the same m, so the quotient is
+    // exact.
+    auto update_max = [&](const float (&mx_lane)[NB]) {
 #pragma unroll
         for (int n = 0; n < NB; ++n) {
-            float mx = -INFINITY;
-#pragma unroll
-            for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[mb][n][v]);
-            mx = halves_max(mx) * c2;
-            // Lazy rescale: the running max m only moves when the tile max
-            // exceeds it by more than 2^RESCALE_LOG2, so most tiles skip the
-            // rescale of O and l (a wave-uniform branch).  Weights stay
-            // <= 2^RESCALE_LOG2; O and l share the same m, so the final
-            // quotient is unchanged.
+            const float mx = halves_max(mx_lane[n]) * c2;
             const bool grow = mx > m[n] + RESCALE_LOG2;
             if (__builtin_amdgcn_ballot_w64(grow)) {
                 const float m_new = grow ? mx : m[n];
@@ -335,99 +417,147 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
 #pragma unroll
                     for (int v = 0; v < 16; ++v) o[n][md][v] *= alpha;
             }
-            const float m_use = (m[n] == -INFINITY) ? 0.f : m[n];
-            float rs = 0.f;
+        }
+    };
+    auto max_shift = [&](float (&m_use)[NB]) {
+#pragma unroll
+        for (int n = 0; n < NB; ++n) m_use[n] = (m[n] == -INFINITY) ? 0.f : m[n];
+    };
+    // S^T[key][query] = K Q^T for the 64 keys of a stage x this wave's
+    // 32 * NB queries.  Each step is fenced so the reads stay two steps ahead
+    // of their MFMAs.
+    auto qk = [&](uint32_t soff, Tile &sn) {
+        const uint32_t kb = kbase + soff;
+#pragma unroll
+        for (int n = 0; n < NB; ++n)
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const float p = fast_exp2(__builtin_fmaf(s[mb][n][v], c2, -m_use));
-                    s[mb][n][v] = p;
-                    rs += p;
-                }
-            l[n] += rs;
+                for (int v = 0; v < 16; ++v) sn[n][mb][v] = 0.f;
+        bf16x8 kf[3];
+        kf[0] = kread(kb, 0);
+        kf[1] = kread(kb, 1);
 #pragma unroll
-            for (int ks4 = 0; ks4 < 4; ++ks4)
+        for (int i = 0; i < NQK; ++i) {
+            if (i + 2 < NQK) kf[(i + 2) % 3] = kread(kb, i + 2);
 #pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    pf[n][ks4][e] = (__bf16)s[ks4 >> 1][n][8 * (ks4 & 1) + e];
+            for (int n = 0; n < NB; ++n)
+                sn[n][i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[n][i >> 1], sn[n][i & 1], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
         }
-
-        // O^T[d][query] += V^T P^T; V^T fragments by LDS transpose reads
-        const int j16 = lane & 15;
-        const int dsub = 16 * ((lane >> 4) & 1) + 4 * (j16 & 3);
-#pragma unroll
-        for (int ks4 = 0; ks4 < 4; ++ks4) {
-            const int k0 = 16 * ks4 + 4 * hf + (j16 >> 2);
-#pragma unroll
-            for (int md = 0; md < MD; ++md) {
-                const int dcol = 32 * md + dsub;
-                const i16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (lds_i16x4 *)(vs + k0 * VP + dcol * 2));
-                const i16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (lds_i16x4 *)(vs + (k0 + 8) * VP + dcol * 2));
-                // whole-vector reinterpretation: element-wise bf16 casts of
-                // the transpose-read result were lowered to a splat
-                const bf16x8 vfrag = __builtin_bit_cast(
-                    bf16x8, __builtin_shufflevector(va, vb, 0, 1, 2, 3, 4, 5, 6, 7));
-#pragma unroll
-                for (int n = 0; n < NB; ++n)
-                    o[n][md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag, pf[n][ks4], o[n][md], 0, 0, 0);
-            }
+    };
+    // softmax of a tile: mask, running max, P weights and their sum
+    auto softmax = [&](int t, Tile &sc, bf16x8 (&pf)[NB][4]) {
+        if ((t + 1) * KT > kfull) {
+            // (a real branch: the compiler would otherwise turn this rare
+            // path into selects executed on every tile)
+            asm volatile("" ::: "memory");
+            mask(t, sc);
         }
-
+        float mx[NB];
+        lane_max(sc, mx);
+        update_max(mx);
+        float m_use[NB];
+        max_shift(m_use);
+        float lp[NB][2];
+#pragma unroll
+        for (int n = 0; n < NB; ++n) lp[n][0] = lp[n][1] = 0.f;
+#pragma unroll
+        for (int e = 0; e < 32 * NB; e += 2) softmax_pair(sc, pf, e, m_use, lp[e >> 5][(e >> 1) & 1]);
+#pragma unroll
+        for (int n = 0; n < NB; ++n) l[n] += lp[n][0] + lp[n][1];
+    };
+    // O^T[d][query] += V^T P^T from the V tile of a stage; V reads two steps
+    // ahead of their MFMAs
+    auto pv = [&](uint32_t soff, const bf16x8 (&pf)[NB][4]) {
+        const uint32_t v0 = vbase[0] + soff, v1 = vbase[1] + soff;
+        bf16x8 vf[3];
+        vf[0] = vread(v0, v1, 0);
+        vf[1] = vread(v0, v1, 1);
+#pragma unroll
+        for (int i = 0; i < NPV; ++i) {
+            if (i + 2 < NPV) vf[(i + 2) % 3] = vread(v0, v1, i + 2);
+#pragma unroll
+            for (int n = 0; n < NB; ++n)
+                o[n][i % MD] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i % 3], pf[n][i / MD], o[n][i % MD], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+        }
     };
 
-    // Pipeline: tile t is computed from LDS buffer (t - t_begin) & 1 while
-    // the loads of tiles t+1 and t+2 are in flight in the two register sets;
-    // after the compute, tile t+1 is stored to the other buffer and the loads
-    // of tile t+3 are issued.  One barrier per tile.  Unrolled by two so the
-    // register set of every step is fixed at compile time.
-    // Prologue: only the first tile is requested before the first compute,
-    // so it is not queued behind the next tiles of every other work-group;
-    // tiles 1 and 2 stream in while tile 0 is computed.
-    if (t_begin < t_end) {
-        load_tile(t_begin * KT, pg0, kA, vA);
-        store_tile(0, kA, vA);
-        if (t_begin + 1 < t_end) load_tile((t_begin + 1) * KT, pg1, kB, vB);
-        if (t_begin + 2 < t_end) load_tile((t_begin + 2) * KT, pg2, kA, vA);
-    }
+    // ---- pipeline ---------------------------------------------------------
+    // Tile t lives in ring stage (t - t_begin) % NSTAGE.  Every wave runs
+    // the same loop: step j is an MFMA block (O += P V of tile j-1, then S^T
+    // of tile j), a work-group barrier, the VALU block (softmax of tile j)
+    // and another barrier.  The second wave on each SIMD (waves NWD..NW-1,
+    // SIMD = wave % 4) enters the loop one barrier late, so on every SIMD one
+    // wave's softmax overlaps the other wave's MFMAs.  The leading waves
+    // issue the loads of tile j+2 at the start of step j and wait for tile
+    // j+1 before its last barrier: a stage is refilled only after the
+    // trailing waves' last read of its tile, and its loads have two steps to
+    // land.
+    static_assert(NW == 8, "two waves per SIMD");
+    const bool lead = wave < NWD;
+    Tile S;
+    bf16x8 pf[NB][4];
+    const int n_tiles = t_end - t_begin;
+    auto stage_off = [&](int t) -> uint32_t { return (uint32_t)((t - t_begin) % NSTAGE) * TILEB; };
+    if (n_tiles > 0) {
+        if (lead) {
+            issue_tile(t_begin, 0, pg0);
+            if (n_tiles > 1) issue_tile(t_begin + 1, 1, pg1);
+            wait_tiles(min(n_tiles - 1, 1));
+        }
 #pragma unroll
-    for (int k = 0; k < PAGE_LDS / NT; ++k)
-        if (tid + k * NT < n_lds_pages) page_lds[tid + k * NT] = pre[k];
-    if (app_first) {
-        const int64_t dst = app_dst(app_page, app_pos, app_c);
-        *(u32x4 *)(a.kpool + dst) = app_k;
-        *(u32x4 *)(a.vpool + dst) = app_v;
-    }
-    __syncthreads();
-    for (int t = t_begin; t < t_end; t += 2) {
-        compute_tile(0, t * KT);
-        if (t + 1 < t_end) store_tile(1, kB, vB);
-        if (t + 3 < t_end) load_tile((t + 3) * KT, page_of(t + 3), kB, vB);
-        __syncthreads();
-        if (t + 1 >= t_end) break;
-        compute_tile(1, (t + 1) * KT);
-        if (t + 2 < t_end) store_tile(0, kA, vA);
-        if (t + 4 < t_end) load_tile((t + 4) * KT, page_of(t + 4), kA, vA);
-        __syncthreads();
-    }
-
-    // fused append, remaining rounds (more chunks than threads)
-    for (int u = tid + NT; u < app_n; u += NT) {
-        int64_t sk, sv;
-        int pos, c;
-        app_src(u, sk, sv, pos, c);
-        const int64_t dst = app_dst(ptab[pos >> 6], pos, c);
-        *(u32x4 *)(a.kpool + dst) = *(const u32x4 *)(a.kc + sk);
-        *(u32x4 *)(a.vpool + dst) = *(const u32x4 *)(a.vc + sv);
+        for (int k = 0; k < PAGE_LDS / NT; ++k)
+            if (tid + k * NT < n_lds_pages) page_lds[tid + k * NT] = pre[k];
+        wg_barrier();
+        int pg_next = pg2;   // page of tile j+2, read one step ahead
+        if (!lead) wg_barrier();
+        for (int j = t_begin; j <= t_end; ++j) {
+            // Addresses derived from these per-lane bases are cheap to
+            // recompute; hidden from the optimiser here so that it does not
+            // hoist them out of the loop and hold them in registers the
+            // pipeline needs.
+            asm volatile("" : "+v"(kbase), "+v"(vbase[0]), "+v"(vbase[1]), "+v"(lofs_p), "+v"(lofs_k), "+v"(lofs_v));
+            if (lead && j + 2 < t_end) {
+                issue_tile(j + 2, (j + 2 - t_begin) % NSTAGE, pg_next);
+                if (j + 3 < t_end) pg_next = page_of(j + 3);
+            }
+            if (j > t_begin) pv(stage_off(j - 1), pf);
+            if (j < t_end) qk(stage_off(j), S);
+            wg_barrier();
+            if (j < t_end) softmax(j, S, pf);
+            if (lead && j + 1 < t_end) wait_tiles(j + 2 < t_end ? 1 : 0);
+            wg_barrier();
+        }
+        if (lead) wg_barrier();
     }
 
-    // ---- epilogue -------------------------------------------------------
+    // ---- fused append -----------------------------------------------------
+    // The G query heads of a group share one KV head, so only the items of
+    // its first head write; they split the new tokens evenly among them.
+    // This kernel reads the new block from kc/vc, never from the slots being
+    // written, so the append can trail the attention.
+    if (step && a.fuse_append && hh == 0) {
+        constexpr int CH = D / 8;
+        const int napp = a.nqt * a.nsplit;
+        const int ai = qi * a.nsplit + split;
+        const int s0 = (int)((int64_t)ai * a.Lq / napp);
+        const int n = ((int)((int64_t)(ai + 1) * a.Lq / napp) - s0) * CH;
+        for (int u = tid; u < n; u += NT) {
+            const int t = s0 + u / CH, c = u % CH;
+            const int pos = n_pool + t;
+            const int64_t dst = (((int64_t)ptab[pos >> 6] * a.Hkv + kvh) * KT + (pos & 63)) * D + 8 * c;
+            *(u32x4 *)(a.kpool + dst) = *(const u32x4 *)(a.kc + b * a.kc_sb + (int64_t)t * a.kc_st + kvh * a.kc_sh + 8 * c);
+            *(u32x4 *)(a.vpool + dst) = *(const u32x4 *)(a.vc + b * a.vc_sb + (int64_t)t * a.vc_st + kvh * a.vc_sh + 8 * c);
+        }
+    }
+
+    // ---- epilogue -----------------------------------------------------------
 #pragma unroll
     for (int n = 0; n < NB; ++n) {
         const float lt = halves_sum(l[n]);
-        const int r = rows[n];
+        const int r = row[n];
         if (r >= a.Lq) continue;
         if (a.nsplit == 1) {
             const float inv = lt > 0.f ? 1.f / lt : 0.f;
@@ -557,10 +687,10 @@ __global__ __launch_bounds__(256) void append_kernel(const AppendArgs a) {
     }
 }
 
-template <int D, int NB, int NW>
+template <int D, int NW, int NB>
 int launch_attn_t(const AttnArgs &a, hipStream_t st) {
     const int grid = a.per_xcd * NUM_XCD;
-    hipLaunchKernelGGL((attn_kernel<D, NB, NW>), dim3(grid), dim3(NW * 64), 0, st, a);
+    hipLaunchKernelGGL((attn_kernel<D, NW, NB>), dim3(grid), dim3(NW * 64), 0, st, a);
     return (int)hipGetLastError();
 }
 
@@ -568,14 +698,9 @@ int launch_attn_t(const AttnArgs &a, hipStream_t st) {
 
 int launch_attention(const AttnArgs &a, int head_dim, TileShape shape, void *stream) {
     hipStream_t st = (hipStream_t)stream;
-    if (shape.nb != 1) return (int)hipErrorInvalidValue;
-    if (head_dim == 128) {
-        if (shape.nw == 4) return launch_attn_t<128, 1, 4>(a, st);
-        if (shape.nw == 8) return launch_attn_t<128, 1, 8>(a, st);
-    } else if (head_dim == 64) {
-        if (shape.nw == 4) return launch_attn_t<64, 1, 4>(a, st);
-        if (shape.nw == 8) return launch_attn_t<64, 1, 8>(a, st);
-    }
+    if (shape.nw != 8 || shape.nb != 1) return (int)hipErrorInvalidValue;
+    if (head_dim == 128) return launch_attn_t<128, 8, 1>(a, st);
+    if (head_dim == 64) return launch_attn_t<64, 8, 1>(a, st);
     return (int)hipErrorInvalidValue;
 }
 
