@@ -124,14 +124,32 @@ __device__ __forceinline__ int swz(int r) {
     else return 4 * ((r >> 1) & 1) + ((r >> 2) & 3);                // 128-byte rows, two per bank line
 }
 
-typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) char lds_char;
 
-
-// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane;
-// lds must be the same for the whole wave.
-__device__ __forceinline__ void dma16(const void *g, char *lds) {
-    __builtin_amdgcn_global_load_lds(g, (lds_void *)lds, 16, 0, 0);
+// LDS byte address of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_addr(const char *p) {
+    return (uint32_t)(uintptr_t)(const lds_char *)p;
 }
+
+// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane
+// (lds wave-uniform, in M0).  Written as inline assembly on purpose: with the
+// load-to-LDS builtin in a loop the compiler's wait-count model turns every
+// later LDS-read wait into a full drain (lgkmcnt(0)), which serialises the
+// MFMA blocks.  These loads are invisible to that model; the kernel waits
+// for them itself (wait_vm_lgkm before each barrier that publishes a tile).
+// M0 is written here; no other code in this file uses M0, so clobbering it
+// is safe (clang warns because M0 is a reserved register).
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+// Per-lane 64-bit address:
+__device__ __forceinline__ void dma16(const char *g, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" :: "v"(g), "s"(lds) : "memory", "m0");
+}
+// Wave-uniform base + per-lane 32-bit byte offset:
+__device__ __forceinline__ void dma16s(const char *base, uint32_t off, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" :: "v"(off), "s"(base), "s"(lds) : "memory", "m0");
+}
+#pragma clang diagnostic pop
 
 template <int D, int NW, int NB>
 __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
@@ -212,18 +230,23 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     const int pg0 = page_glb(t_begin), pg1 = page_glb(t_begin + 1), pg2 = page_glb(t_begin + 2);
 
     // ---- this lane's query rows -------------------------------------------
-    // row n of the lane: q0 + wave * 32 * NB + 32 * n + l32
+    // row n of the lane: q0 + wave * 32 * NB + 32 * n + l32 (the fragments
+    // are loaded after the first tile loads are issued, below)
     int row[NB], kend[NB];
     bf16x8 qf[NB][KK];
 #pragma unroll
     for (int n = 0; n < NB; ++n) {
         row[n] = q0 + wave * 32 * NB + 32 * n + l32;
-        const int rc = min(row[n], a.Lq - 1);
-        kend[n] = step ? k_hi : block_end<false>(offs, a.nb, rc);
-        const uint16_t *qp = a.q + b * a.q_sb + (int64_t)rc * a.q_st + hq * a.q_sh + 8 * hf;
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) qf[n][kk] = *(const bf16x8 *)(qp + 16 * kk);
+        kend[n] = step ? k_hi : block_end<false>(offs, a.nb, min(row[n], a.Lq - 1));
     }
+    auto load_q = [&]() {
+#pragma unroll
+        for (int n = 0; n < NB; ++n) {
+            const uint16_t *qp = a.q + b * a.q_sb + (int64_t)min(row[n], a.Lq - 1) * a.q_st + hq * a.q_sh + 8 * hf;
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) qf[n][kk] = *(const bf16x8 *)(qp + 16 * kk);
+        }
+    };
 
     // ---- direct-to-LDS tile loads -----------------------------------------
     // The leading waves (wave < NWD) load the tiles.  Wave-wide load i of
@@ -246,50 +269,83 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     uint32_t lofs_p = (uint32_t)(lrow0 * ROWB + 16 * lch);
     uint32_t lofs_k = (uint32_t)((lane / LPR) * kst2 + 16 * lch);
     uint32_t lofs_v = (uint32_t)((lane / LPR) * vst2 + 16 * lch);
-    // issue the loads of tile u (its physical page, if cached, is `page`,
-    // wave-uniform) into ring stage s: NI wave-wide loads for K and for V
-    auto issue_tile = [&](int u, int s, int page) {
+    // Loads of one tile u (its physical page, if cached, is `page`,
+    // wave-uniform) into ring stage s: NI wave-wide loads for K and for V.
+    // A tile inside one cache page or inside the contiguous keys is loaded
+    // from a wave-uniform base + i * step and a per-lane offset, so its loads
+    // can be spread out (issue_part); a tile straddling the cache end or the
+    // last key is loaded at once with per-lane addresses (issue_straddle).
+    struct TileLoad {
+        const char *bk, *bv;   // wave-uniform bases of load 0
+        int64_t sk, sv;        // base step per load
+        uint32_t ok, ov;       // per-lane byte offsets
+        uint32_t kd, vd;       // LDS destination of load 0 of this wave
+        bool straddle;
+    };
+    auto plan_tile = [&](int u, int s, int page) -> TileLoad {
         const int kt = u * KT;
-        char *kd = smem + s * TILEB + wave * 1024;
-        char *vd = smem + VRING + s * TILEB + wave * 1024;
-        const int64_t tb = ((int64_t)page * a.Hkv + kvh) * TILEB;
-        const char *kg = kpool_b + tb, *vg = vpool_b + tb;
+        TileLoad t;
+        t.kd = lds_addr(smem) + s * TILEB + wave * 1024;
+        t.vd = t.kd + VRING;
+        t.straddle = false;
         if (kt + KT <= n_pool) {
             // whole tile in one cache page
-#pragma unroll
-            for (int i = 0; i < NI; ++i) {
-                dma16(kg + i * NWD * 1024 + lofs_p, kd + i * NWD * 1024);
-                dma16(vg + i * NWD * 1024 + lofs_p, vd + i * NWD * 1024);
-            }
+            const int64_t tb = ((int64_t)page * a.Hkv + kvh) * TILEB;
+            t.bk = kpool_b + tb;
+            t.bv = vpool_b + tb;
+            t.sk = t.sv = NWD * 1024;
+            t.ok = t.ov = lofs_p;
         } else if (kt >= n_pool && kt + KT <= k_hi) {
             // whole tile in the contiguous keys
             const int64_t j0 = kt - n_pool + wave * RPW;
-#pragma unroll
-            for (int i = 0; i < NI; ++i) {
-                const int64_t j = j0 + i * NWD * RPW;
-                dma16(kc_b + j * kst2 + lofs_k, kd + i * NWD * 1024);
-                dma16(vc_b + j * vst2 + lofs_v, vd + i * NWD * 1024);
-            }
+            t.bk = kc_b + j0 * kst2;
+            t.bv = vc_b + j0 * vst2;
+            t.sk = NWD * RPW * kst2;
+            t.sv = NWD * RPW * vst2;
+            t.ok = lofs_k;
+            t.ov = lofs_v;
         } else {
-            // the tile straddles the cache end or runs past the last key:
-            // rows past the end repeat the last key (their scores are masked)
-            const int64_t c0 = (int64_t)(kt - n_pool);   // contiguous row of the tile's first key
-            const char *kcg = kc_b + c0 * kst2, *vcg = vc_b + c0 * vst2;
-            const uint32_t lofs_c = lofs_p - lrow0 * ROWB;   // the chunk's byte offset in a row
+            t.straddle = true;
+        }
+        return t;
+    };
+    auto issue_part = [&](const TileLoad &t, int i) {
+        dma16s(t.bk + i * t.sk, t.ok, t.kd + i * NWD * 1024);
+        dma16s(t.bv + i * t.sv, t.ov, t.vd + i * NWD * 1024);
+    };
+    // rows past the end repeat the last key (their scores are masked)
+    auto issue_straddle = [&](int u, int s, int page) {
+        const int kt = u * KT;
+        const uint32_t kd = lds_addr(smem) + s * TILEB + wave * 1024;
+        const uint32_t vd = kd + VRING;
+        const int64_t tb = ((int64_t)page * a.Hkv + kvh) * TILEB;
+        const char *kg = kpool_b + tb, *vg = vpool_b + tb;
+        const int64_t c0 = (int64_t)(kt - n_pool);   // contiguous row of the tile's first key
+        const char *kcg = kc_b + c0 * kst2, *vcg = vc_b + c0 * vst2;
+        const uint32_t lofs_c = lofs_p - lrow0 * ROWB;   // the chunk's byte offset in a row
 #pragma unroll
-            for (int i = 0; i < NI; ++i) {
-                const int r = min(lrow0 + i * NWD * RPW, k_hi - 1 - kt);   // row within the tile
-                const char *gk, *gv;
-                if (kt + r < n_pool) {
-                    gk = kg + (uint32_t)(r * ROWB) + lofs_c;
-                    gv = vg + (uint32_t)(r * ROWB) + lofs_c;
-                } else {
-                    gk = kcg + (uint32_t)(r * kst2) + lofs_c;
-                    gv = vcg + (uint32_t)(r * vst2) + lofs_c;
-                }
-                dma16(gk, kd + i * NWD * 1024);
-                dma16(gv, vd + i * NWD * 1024);
+        for (int i = 0; i < NI; ++i) {
+            const int r = min(lrow0 + i * NWD * RPW, k_hi - 1 - kt);   // row within the tile
+            const char *gk, *gv;
+            if (kt + r < n_pool) {
+                gk = kg + (uint32_t)(r * ROWB) + lofs_c;
+                gv = vg + (uint32_t)(r * ROWB) + lofs_c;
+            } else {
+                gk = kcg + (uint32_t)(r * kst2) + lofs_c;
+                gv = vcg + (uint32_t)(r * vst2) + lofs_c;
             }
+            dma16(gk, kd + i * NWD * 1024);
+            dma16(gv, vd + i * NWD * 1024);
+        }
+    };
+    // all loads of tile u at once
+    auto issue_tile = [&](int u, int s, int page) {
+        const TileLoad t = plan_tile(u, s, page);
+        if (t.straddle) {
+            issue_straddle(u, s, page);
+        } else {
+#pragma unroll
+            for (int i = 0; i < NI; ++i) issue_part(t, i);
         }
         // the waits count this tile's loads as one group: keep later memory
         // operations from being moved in between
@@ -361,18 +417,27 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     // in P's B-operand order (fragment ks4 = e % 32 / 8 holds keys
     // 8 * (ks4 & 1) + e % 8 of key block ks4 / 2)
     auto score = [&](const Tile &sc, int e) -> float { return sc[e >> 5][(e >> 4) & 1][e & 15]; };
-    // P weights of scores e and e+1: 2^(s * c2 - m), rounded to bf16 for
-    // P.V; l accumulates them in fp32 (so lse is exact to fp32 rounding)
-    auto softmax_pair = [&](const Tile &sc, bf16x8 (&pf)[NB][4], int e, const float (&m_use)[NB],
-                            float &lacc) {
-        const int n = e >> 5, f = e & 31;
-        const float x0 = fast_exp2(__builtin_fmaf(score(sc, e), c2, -m_use[n]));
-        const float x1 = fast_exp2(__builtin_fmaf(score(sc, e + 1), c2, -m_use[n]));
-        pf[n][f >> 3][f & 7] = (__bf16)x0;
-        pf[n][f >> 3][(f & 7) + 1] = (__bf16)x1;
-        lacc += x0;
-        lacc += x1;
-        asm volatile("" : "+v"(lacc));   // keep the sum beside its exps
+    // P weights of a tile: 2^(s * c2 - m), rounded to bf16 for P.V, and their
+    // fp32 row sums (so lse is exact to fp32 rounding).  One straight block:
+    // all exponents, then all exps, then the packs and a pairwise sum, so
+    // the dependent steps of different scores overlap.
+    auto softmax_weights = [&](const Tile &sc, bf16x8 (&pf)[NB][4], const float (&m_use)[NB]) {
+#pragma unroll
+        for (int n = 0; n < NB; ++n) {
+            float x[32];
+#pragma unroll
+            for (int f = 0; f < 32; ++f) x[f] = __builtin_fmaf(score(sc, 32 * n + f), c2, -m_use[n]);
+#pragma unroll
+            for (int f = 0; f < 32; ++f) x[f] = fast_exp2(x[f]);
+#pragma unroll
+            for (int f = 0; f < 32; ++f) pf[n][f >> 3][f & 7] = (__bf16)x[f];
+            // pairwise sum in a fixed order (the same for every tile)
+#pragma unroll
+            for (int w = 1; w < 32; w *= 2)
+#pragma unroll
+                for (int f = 0; f < 32; f += 2 * w) x[f] += x[f + w];
+            l[n] += x[0];
+        }
     };
     // in-lane max of a tile's scores per query block; the other half-wave's
     // keys are folded in by update_max
@@ -459,13 +524,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
         update_max(mx);
         float m_use[NB];
         max_shift(m_use);
-        float lp[NB][2];
-#pragma unroll
-        for (int n = 0; n < NB; ++n) lp[n][0] = lp[n][1] = 0.f;
-#pragma unroll
-        for (int e = 0; e < 32 * NB; e += 2) softmax_pair(sc, pf, e, m_use, lp[e >> 5][(e >> 1) & 1]);
-#pragma unroll
-        for (int n = 0; n < NB; ++n) l[n] += lp[n][0] + lp[n][1];
+        softmax_weights(sc, pf, m_use);
     };
     // O^T[d][query] += V^T P^T from the V tile of a stage; V reads two steps
     // ahead of their MFMAs
@@ -505,8 +564,13 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
         if (lead) {
             issue_tile(t_begin, 0, pg0);
             if (n_tiles > 1) issue_tile(t_begin + 1, 1, pg1);
-            wait_tiles(min(n_tiles - 1, 1));
         }
+        load_q();
+        // Everything in flight lands here (the first two tiles, the query
+        // fragments, the staged page ids).  Settling all vector loads before
+        // the loop also keeps the compiler from placing waits for the query
+        // loads inside it, where they would drain the tile pipeline.
+        wait_vm_lgkm<0>();
 #pragma unroll
         for (int k = 0; k < PAGE_LDS / NT; ++k)
             if (tid + k * NT < n_lds_pages) page_lds[tid + k * NT] = pre[k];
@@ -519,14 +583,16 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
             // hoist them out of the loop and hold them in registers the
             // pipeline needs.
             asm volatile("" : "+v"(kbase), "+v"(vbase[0]), "+v"(vbase[1]), "+v"(lofs_p), "+v"(lofs_k), "+v"(lofs_v));
-            if (lead && j + 2 < t_end) {
-                issue_tile(j + 2, (j + 2 - t_begin) % NSTAGE, pg_next);
-                if (j + 3 < t_end) pg_next = page_of(j + 3);
-            }
             if (j > t_begin) pv(stage_off(j - 1), pf);
             if (j < t_end) qk(stage_off(j), S);
             wg_barrier();
+            // the leading waves issue the loads of tile j+2 here, ahead of
+            // their softmax, rather than ahead of their MFMA block
+            if (lead && j + 2 < t_end) issue_tile(j + 2, (j + 2 - t_begin) % NSTAGE, pg_next);
             if (j < t_end) softmax(j, S, pf);
+            // (read here, under the wait below: a scalar or LDS read left in
+            // flight across the MFMA block would force full LDS drains there)
+            if (lead && j + 3 < t_end) pg_next = page_of(j + 3);
             if (lead && j + 1 < t_end) wait_tiles(j + 2 < t_end ? 1 : 0);
             wg_barrier();
         }
