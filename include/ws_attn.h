@@ -24,7 +24,10 @@
  * - Token tensors are 4-d [batch][tokens][heads][head_dim] described by
  *   ws_tensor4: the head_dim axis is contiguous; the three other strides are
  *   in ELEMENTS.  Pointers must be 16-byte aligned and strides multiples of
- *   8 elements (128-bit loads).
+ *   8 elements (128-bit loads).  The keys and values read by the attention
+ *   entry points (k_new / v_new of a step, k / v of a prefill) must have a
+ *   token stride below 2^24 elements (WS_ERR_SHAPE otherwise): the kernels
+ *   address a tile of them with 32-bit offsets.
  * - All device pointers are HIP device memory of the current device; the
  *   caller owns every buffer (inputs, outputs, cache pool, page tables,
  *   workspace).  The library allocates no device memory and keeps no state

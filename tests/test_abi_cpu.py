@@ -100,6 +100,11 @@ def test_step_errors(lib):
     assert step_call(lib, h, q=t4(ptr=FAKE + 2)) == 4                  # misaligned pointer
     assert step_call(lib, h, q=t4(sb=16 * 4 * 128, st=4 * 128, sh=130)) == 4  # stride % 8
     assert step_call(lib, h, lse=FAKE + 2) == 4
+    big = 1 << 24                                                      # K/V token stride limit
+    assert step_call(lib, h, kn=t4(H=2, sb=big, st=big, sh=128)) == 2
+    assert step_call(lib, h, vn=t4(H=2, sb=big, st=big, sh=128)) == 2
+    # just below the limit passes the stride check and fails a later one
+    assert step_call(lib, h, kn=t4(H=2, sb=big, st=big - 8, sh=128), lse=FAKE + 2) == 4
     assert step_call(lib, h, Hq=3, q=t4(H=3), out=t4(H=3)) == 8        # Hq % Hkv
     h2 = Host(lens=(10, 300))                                          # 300 > 4 pages * 64
     assert step_call(lib, h2) == 7
@@ -169,6 +174,9 @@ def test_prefill_errors(lib):
     null = ws.Tensor4(None, 1, 0, 0, 0)
     assert prefill_call(lib, [[0, 8]], k=null, v=null) == 1       # paged without a cache
     assert prefill_call(lib, [[0, 8]], Hq=0) == 2
+    big = 1 << 24
+    assert prefill_call(lib, [[0, 8]], k=t4(H=2, L=8, sb=big, st=big, sh=128)) == 2
+    assert prefill_call(lib, [[0, 8]], v=t4(H=2, L=8, sb=big, st=big, sh=128)) == 2
     h = Host(B=1, lens=(0,))
     assert prefill_call(lib, [[0, 300]], k=null, v=null, desc=h.desc()) == 7
     h.table[0, 2] = 77
