@@ -217,21 +217,15 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     const int tp_end = min(t_end, (n_pool + KT - 1) / KT);   // tiles with cache rows
     auto page_glb = [&](int t) -> int { return t < tp_end ? ld_uniform(ptab, t) : 0; };
     const int n_lds_pages = min(max(tp_end - t_begin, 0), PAGE_LDS);
-    int pre[PAGE_LDS / NT];
-#pragma unroll
-    for (int k = 0; k < PAGE_LDS / NT; ++k) {
-        const int i = tid + k * NT;
-        pre[k] = i < n_lds_pages ? ptab[t_begin + i] : 0;
-    }
     auto page_of = [&](int t) -> int {
         const int i = t - t_begin;
         return i < PAGE_LDS ? __builtin_amdgcn_readfirstlane(page_lds[i]) : page_glb(t);
     };
-    const int pg0 = page_glb(t_begin), pg1 = page_glb(t_begin + 1), pg2 = page_glb(t_begin + 2);
 
     // ---- this lane's query rows -------------------------------------------
     // row n of the lane: q0 + wave * 32 * NB + 32 * n + l32 (the fragments
-    // are loaded after the first tile loads are issued, below)
+    // are staged through LDS in the pipeline prologue, below)
+    static_assert(NB == 1, "query staging holds 32 rows per wave");
     int row[NB], kend[NB];
     bf16x8 qf[NB][KK];
 #pragma unroll
@@ -239,14 +233,6 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
         row[n] = q0 + wave * 32 * NB + 32 * n + l32;
         kend[n] = step ? k_hi : block_end<false>(offs, a.nb, min(row[n], a.Lq - 1));
     }
-    auto load_q = [&]() {
-#pragma unroll
-        for (int n = 0; n < NB; ++n) {
-            const uint16_t *qp = a.q + b * a.q_sb + (int64_t)min(row[n], a.Lq - 1) * a.q_st + hq * a.q_sh + 8 * hf;
-#pragma unroll
-            for (int kk = 0; kk < KK; ++kk) qf[n][kk] = *(const bf16x8 *)(qp + 16 * kk);
-        }
-    };
 
     // ---- direct-to-LDS tile loads -----------------------------------------
     // The leading waves (wave < NWD) load the tiles.  Wave-wide load i of
@@ -374,6 +360,31 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
         const int vc = 2 * ((lane >> 4) & 1) + ((j16 & 3) >> 1);
         vbase[e] = VRING + vr * ROWB + 16 * (vc ^ swz<D>(vr)) + 8 * (j16 & 1);
     }
+
+    // Query rows of this wave go global -> LDS -> registers: the direct
+    // loads stay in order with the tile loads, so one counted wait covers
+    // both and the first tile can be used while the second is in flight.
+    // They are staged in ring stages 2 and 3 (of the K ring for waves
+    // 0..3, of the V ring for waves 4..7), which are first refilled in loop
+    // step t_begin, after every wave has passed the prologue barrier.  The
+    // layout is that of a key tile, so the fragments are read like K.
+    constexpr int QI = 32 * ROWB / 1024;   // wave-wide loads per wave
+    const uint32_t q_stage = (uint32_t)((wave < 4 ? 0 : VRING) + 2 * TILEB + (wave & 3) * 32 * ROWB);
+    auto issue_q = [&]() {
+        const char *qg = (const char *)(a.q + b * a.q_sb + hq * a.q_sh);
+#pragma unroll
+        for (int i = 0; i < QI; ++i) {
+            const int r = i * RPW + lane / LPR;   // row within the wave's 32
+            const int ch = (lane % LPR) ^ swz<D>(r);
+            const int64_t t = min(q0 + wave * 32 + r, a.Lq - 1);
+            dma16(qg + t * (2 * a.q_st) + 16 * ch, lds_addr(smem) + q_stage + i * 1024);
+        }
+    };
+    auto read_q = [&]() {
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk)
+            qf[0][kk] = *(const bf16x8 *)(smem + q_stage + (kbase ^ (32 * kk)));
+    };
 
     const float c2 = a.scale_log2;
     f32x16 o[NB][MD];
@@ -561,21 +572,41 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     const int n_tiles = t_end - t_begin;
     auto stage_off = [&](int t) -> uint32_t { return (uint32_t)((t - t_begin) % NSTAGE) * TILEB; };
     if (n_tiles > 0) {
+        // Prologue: every wave loads its query rows; the leading waves then
+        // issue the first two tiles and wait for the first (the second stays
+        // in flight into loop step t_begin, as in the steady state); the
+        // trailing waves stage the split's page ids in LDS.  The page-id
+        // reads are the only loads the compiler sees here, so its own waits
+        // never cover the tile loads.
+        issue_q();
+        int pg_next = 0;   // page of tile j+2, read one step ahead
         if (lead) {
+            const int pg0 = page_glb(t_begin), pg1 = page_glb(t_begin + 1);
+            pg_next = page_glb(t_begin + 2);
             issue_tile(t_begin, 0, pg0);
-            if (n_tiles > 1) issue_tile(t_begin + 1, 1, pg1);
-        }
-        load_q();
-        // Everything in flight lands here (the first two tiles, the query
-        // fragments, the staged page ids).  Settling all vector loads before
-        // the loop also keeps the compiler from placing waits for the query
-        // loads inside it, where they would drain the tile pipeline.
-        wait_vm_lgkm<0>();
+            if (n_tiles > 1) {
+                issue_tile(t_begin + 1, 1, pg1);
+                wait_vm_lgkm<2 * NI>();
+            } else {
+                wait_vm_lgkm<0>();
+            }
+        } else {
+            constexpr int NPT = PAGE_LDS / (NT / 2);
+            const int ti = tid - NT / 2;
+            int pre[NPT];
 #pragma unroll
-        for (int k = 0; k < PAGE_LDS / NT; ++k)
-            if (tid + k * NT < n_lds_pages) page_lds[tid + k * NT] = pre[k];
+            for (int k = 0; k < NPT; ++k) {
+                const int i = ti + k * (NT / 2);
+                pre[k] = i < n_lds_pages ? ptab[t_begin + i] : 0;
+            }
+            wait_vm_lgkm<0>();
+#pragma unroll
+            for (int k = 0; k < NPT; ++k)
+                if (ti + k * (NT / 2) < n_lds_pages) page_lds[ti + k * (NT / 2)] = pre[k];
+        }
+        read_q();
+        wait_vm_lgkm<63>();   // (LDS reads and writes complete; no vector-memory wait)
         wg_barrier();
-        int pg_next = pg2;   // page of tile j+2, read one step ahead
         if (!lead) wg_barrier();
         for (int j = t_begin; j <= t_end; ++j) {
             // Addresses derived from these per-lane bases are cheap to
