@@ -32,8 +32,11 @@ struct AttnArgs {
     int32_t out_f32;
     float *lse;
     // split-KV partials, in blocks of 32 query rows (nrb = ceil(Lq / 32)
-    // blocks per (b, hq)): o [S][B][Hq][nrb][D/4][64 lanes][4] f32 in the
-    // accumulator's register order; (m, l) [S][B][Hq][nrb * 32][2]
+    // blocks per (b, hq)).  f32 output: o [S][B][Hq][nrb][D/4][64 lanes][4]
+    // f32 unnormalised, in the accumulator's register order, and (m, l)
+    // [S][B][Hq][nrb * 32][2].  bf16 output: o / l as bf16
+    // [S][B][Hq][nrb][D/8][64 lanes][8] in register order (two accumulator
+    // groups per lane) and m + log2(l) [S][B][Hq][nrb * 32] f32 at part_ml.
     float *part_o, *part_ml;
     int32_t nrb;
     int32_t B, Lq, Hq, Hkv, G;

@@ -630,26 +630,6 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
         if (lead) wg_barrier();
     }
 
-    // ---- fused append -----------------------------------------------------
-    // The G query heads of a group share one KV head, so only the items of
-    // its first head write; they split the new tokens evenly among them.
-    // This kernel reads the new block from kc/vc, never from the slots being
-    // written, so the append can trail the attention.
-    if (step && a.fuse_append && hh == 0) {
-        constexpr int CH = D / 8;
-        const int napp = a.nqt * a.nsplit;
-        const int ai = qi * a.nsplit + split;
-        const int s0 = (int)((int64_t)ai * a.Lq / napp);
-        const int n = ((int)((int64_t)(ai + 1) * a.Lq / napp) - s0) * CH;
-        for (int u = tid; u < n; u += NT) {
-            const int t = s0 + u / CH, c = u % CH;
-            const int pos = n_pool + t;
-            const int64_t dst = (((int64_t)ptab[pos >> 6] * a.Hkv + kvh) * KT + (pos & 63)) * D + 8 * c;
-            *(u32x4 *)(a.kpool + dst) = *(const u32x4 *)(a.kc + b * a.kc_sb + (int64_t)t * a.kc_st + kvh * a.kc_sh + 8 * c);
-            *(u32x4 *)(a.vpool + dst) = *(const u32x4 *)(a.vc + b * a.vc_sb + (int64_t)t * a.vc_st + kvh * a.vc_sh + 8 * c);
-        }
-    }
-
     // ---- epilogue -----------------------------------------------------------
 #pragma unroll
     for (int n = 0; n < NB; ++n) {
@@ -683,6 +663,25 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
             }
             if (a.lse && hf == 0)
                 a.lse[((int64_t)b * a.Hq + hq) * a.Lq + r] = (m[n] + __builtin_amdgcn_logf(lt)) * 0.69314718055994531f;
+        } else if (!a.out_f32) {
+            // bf16 output: o / l rounded to bf16 and the split's log2-domain
+            // lse; register order, two accumulator groups (16 bytes) per
+            // lane, so each store instruction writes 1 KB contiguous
+            const int64_t blk = (((int64_t)split * a.B + b) * a.Hq + hq) * a.nrb + (r >> 5);
+            const float inv = lt > 0.f ? 1.f / lt : 0.f;
+            uint16_t *op = (uint16_t *)a.part_o + blk * (32 * D) + 8 * lane;
+#pragma unroll
+            for (int pg = 0; pg < 2 * MD; ++pg) {
+                const int md = pg >> 1, g0 = 2 * (pg & 1);
+                u32x4 val;
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    val[2 * h + 0] = pack_bf16x2(o[n][md][4 * (g0 + h) + 0] * inv, o[n][md][4 * (g0 + h) + 1] * inv);
+                    val[2 * h + 1] = pack_bf16x2(o[n][md][4 * (g0 + h) + 2] * inv, o[n][md][4 * (g0 + h) + 3] * inv);
+                }
+                *(u32x4 *)(op + pg * 512) = val;
+            }
+            if (hf == 0) a.part_ml[blk * 32 + l32] = lt > 0.f ? m[n] + __builtin_amdgcn_logf(lt) : -INFINITY;
         } else {
             // register order: each store instruction writes 1 KB contiguous
             const int64_t blk = (((int64_t)split * a.B + b) * a.Hq + hq) * a.nrb + (r >> 5);
@@ -702,6 +701,82 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
             }
         }
     }
+
+    // ---- fused append -----------------------------------------------------
+    // The G query heads of a group share one KV head, so only the items of
+    // its first head write; they split the new tokens evenly among them.
+    // This kernel reads the new block from kc/vc, never from the slots being
+    // written, so the append can trail the attention; it comes after the
+    // epilogue's stores so that its loads overlap their drain.
+    if (step && a.fuse_append && hh == 0) {
+        constexpr int CH = D / 8;
+        const int napp = a.nqt * a.nsplit;
+        const int ai = qi * a.nsplit + split;
+        const int s0 = (int)((int64_t)ai * a.Lq / napp);
+        const int n = ((int)((int64_t)(ai + 1) * a.Lq / napp) - s0) * CH;
+        for (int u = tid; u < n; u += NT) {
+            const int t = s0 + u / CH, c = u % CH;
+            const int pos = n_pool + t;
+            const int64_t dst = (((int64_t)ptab[pos >> 6] * a.Hkv + kvh) * KT + (pos & 63)) * D + 8 * c;
+            *(u32x4 *)(a.kpool + dst) = *(const u32x4 *)(a.kc + b * a.kc_sb + (int64_t)t * a.kc_st + kvh * a.kc_sh + 8 * c);
+            *(u32x4 *)(a.vpool + dst) = *(const u32x4 *)(a.vc + b * a.vc_sb + (int64_t)t * a.vc_st + kvh * a.vc_sh + 8 * c);
+        }
+    }
+}
+
+// bf16 output: split s holds o_s / l_s (bf16) and lse_s = m_s + log2(l_s);
+//   M = max_s lse_s,  L = sum_s 2^(lse_s - M),  o = sum_s 2^(lse_s - M) o_s / L.
+// A thread owns the 8 elements (two accumulator groups) one writer lane
+// stored with one 16-byte store, for every split.
+template <int D>
+__global__ __launch_bounds__(256) void combine16_kernel(const AttnArgs a) {
+    constexpr int MD = D / 32;
+    constexpr int PER_BLK = 2 * MD * 64;      // 16-byte items per 32-row block
+    const int64_t nblk = (int64_t)a.B * a.Hq * a.nrb;
+    const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (u >= nblk * PER_BLK) return;
+    const int64_t blk = u / PER_BLK;
+    const int item = (int)(u % PER_BLK);
+    const int lane = item & 63;
+    const int pg = item >> 6;                 // md * 2 + g0 / 2
+    const int r = (int)(blk % a.nrb) * 32 + (lane & 31);
+    if (r >= a.Lq) return;
+    const int hq = (int)((blk / a.nrb) % a.Hq);
+    const int b = (int)(blk / ((int64_t)a.nrb * a.Hq));
+    const int S = a.nsplit;
+    const float *pl = a.part_ml + blk * 32 + (lane & 31);
+    const uint16_t *po = (const uint16_t *)a.part_o + blk * (32 * D) + pg * 512 + 8 * lane;
+    const int64_t ls = nblk * 32;             // split stride of lse
+    const int64_t ps = nblk * 32 * D;         // split stride of o
+    float M = -INFINITY;
+#pragma unroll 8
+    for (int s = 0; s < S; ++s) M = fmaxf(M, pl[s * ls]);
+    const float Mu = (M == -INFINITY) ? 0.f : M;
+    float L = 0.f;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+    for (int s = 0; s < S; ++s) {
+        const float wgt = __builtin_amdgcn_exp2f(pl[s * ls] - Mu);
+        const u32x4 ov = *(const u32x4 *)(po + s * ps);
+        L += wgt;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            acc[2 * k + 0] += __uint_as_float(ov[k] << 16) * wgt;
+            acc[2 * k + 1] += __uint_as_float(ov[k] & 0xFFFF0000u) * wgt;
+        }
+    }
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+    const int md = pg >> 1, g0 = 2 * (pg & 1), hf = lane >> 5;
+    uint16_t *op = (uint16_t *)a.out + b * a.o_sb + (int64_t)r * a.o_st + hq * a.o_sh + 32 * md + 4 * hf;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        u32x2 val;
+        val[0] = pack_bf16x2(acc[4 * h + 0] * inv, acc[4 * h + 1] * inv);
+        val[1] = pack_bf16x2(acc[4 * h + 2] * inv, acc[4 * h + 3] * inv);
+        *(u32x2 *)(op + 8 * (g0 + h)) = val;
+    }
+    if (a.lse && pg == 0 && lane < 32)
+        a.lse[((int64_t)b * a.Hq + hq) * a.Lq + r] = (M + __builtin_amdgcn_logf(L)) * 0.69314718055994531f;
 }
 
 // Merge the KV-split partials of every query row: with per-split running
@@ -803,6 +878,15 @@ int launch_attention(const AttnArgs &a, int head_dim, TileShape shape, void *str
 
 int launch_combine(const AttnArgs &a, int head_dim, void *stream) {
     hipStream_t st = (hipStream_t)stream;
+    if (!a.out_f32) {
+        const int64_t items = (int64_t)a.B * a.Hq * a.nrb * (head_dim / 32) * 2 * 64;
+        const int64_t grid = (items + 255) / 256;
+        if (head_dim == 128)
+            hipLaunchKernelGGL(combine16_kernel<128>, dim3((unsigned)grid), dim3(256), 0, st, a);
+        else
+            hipLaunchKernelGGL(combine16_kernel<64>, dim3((unsigned)grid), dim3(256), 0, st, a);
+        return (int)hipGetLastError();
+    }
     const int64_t items = (int64_t)a.B * a.Hq * a.nrb * (head_dim / 32) * 4 * 64;
     const int64_t grid = (items + 255) / 256;
     if (head_dim == 128)
