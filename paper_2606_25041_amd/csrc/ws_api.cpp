@@ -147,6 +147,13 @@ bool finish_work(ws::AttnArgs &a) {
     if (n > (int64_t)1 << 30) return false;
     a.n_work = (int32_t)n;
     a.per_xcd = (a.n_work + 7) / 8;
+    a.per_qt = a.G * a.nsplit;
+    a.per_group = a.per_qt * a.nqt;
+    a.fd_group = ws::fastdiv_make((uint32_t)a.per_group);
+    a.fd_qt = ws::fastdiv_make((uint32_t)a.per_qt);
+    a.fd_g = ws::fastdiv_make((uint32_t)a.G);
+    a.fd_hkv = ws::fastdiv_make((uint32_t)a.Hkv);
+    a.fd_split = ws::fastdiv_make((uint32_t)a.nsplit);
     return true;
 }
 

@@ -8,6 +8,28 @@ namespace ws {
 
 enum { MODE_PREFILL = 0, MODE_STEP = 1 };
 
+// Division by a divisor d (1 <= d < 2^31) fixed for a launch, exact for
+// dividends n < 2^31: with l = ceil(log2 d), mul = ceil(2^(31+l) / d) and
+// shift = 31 + l, n / d = (n * mul) >> shift (the round-up method of
+// Granlund and Montgomery, "Division by invariant integers using
+// multiplication", 1994).  mul < 2^32, and the error term n * (mul * d -
+// 2^(31+l)) / 2^(31+l) stays below 1 because n < 2^31 and mul * d -
+// 2^(31+l) < d <= 2^l.
+struct FastDiv {
+    uint32_t mul;
+    uint32_t shift;
+};
+
+inline FastDiv fastdiv_make(uint32_t d) {
+    uint32_t l = 0;
+    while (l < 31 && (1u << l) < d) ++l;
+    const uint64_t num = (uint64_t)1 << (31 + l);
+    FastDiv f;
+    f.mul = (uint32_t)((num + d - 1) / d);
+    f.shift = 31 + l;
+    return f;
+}
+
 // Everything one attention launch needs.  Element strides; bf16 data is
 // carried as uint16_t bit patterns.
 struct AttnArgs {
@@ -47,6 +69,10 @@ struct AttnArgs {
     int32_t nqt;         // q-tiles per (b, hq)
     int32_t n_work;      // B * Hq * nqt * nsplit
     int32_t per_xcd;     // ceil(n_work / 8)
+    int32_t per_group;   // G * nqt * nsplit: work items per (b, KV head)
+    int32_t per_qt;      // G * nsplit: work items per (b, KV head, q-tile)
+    // dividers by per_group, per_qt, G, Hkv and nsplit
+    FastDiv fd_group, fd_qt, fd_g, fd_hkv, fd_split;
     float scale_log2;    // scale * log2(e)
     // step: cache lengths also passed by value when batch <= LENS_IN_ARGS,
     // so the first page lookup does not wait on a load of them

@@ -76,6 +76,11 @@ __device__ __forceinline__ float halves_sum(float x) {
 typedef const __attribute__((address_space(4))) int32_t cint32;
 __device__ __forceinline__ int ld_uniform(const int32_t *p, int64_t i) { return ((const cint32 *)p)[i]; }
 
+// n / d for n < 2^31 with the host-computed divider of d
+__device__ __forceinline__ uint32_t fastdiv(uint32_t n, FastDiv f) {
+    return (uint32_t)(((uint64_t)n * f.mul) >> f.shift);
+}
+
 // End (exclusive) of the block that holds token i: the first offset > i.
 template <bool UNIFORM>
 __device__ __forceinline__ int block_end(const int32_t *off, int nb, int i) {
@@ -169,21 +174,34 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     __shared__ int page_lds[PAGE_LDS];
 
     // ---- work item ------------------------------------------------------
-    const int bid = blockIdx.x;
-    const int w = (bid % NUM_XCD) * a.per_xcd + bid / NUM_XCD;
-    if (w >= a.n_work) return;
-    const int per_group = a.G * a.nqt * a.nsplit;
-    const int group = w / per_group;
-    const int idx = w - group * per_group;
-    const int qi = idx / (a.G * a.nsplit);
-    const int rem = idx - qi * (a.G * a.nsplit);
-    const int split = rem / a.G;
-    const int hh = rem - split * a.G;
-    const int b = group / a.Hkv;
-    const int kvh = group - b * a.Hkv;
-    const int hq = kvh * a.G + hh;
-    const bool step = a.mode == MODE_STEP;
-    const int qt = step ? qi : (a.nqt - 1 - qi);  // prefill: heaviest tiles first
+    // The launch parameters the decode and the query loads need are read in
+    // one batch (the asm makes them all live at once, so the compiler issues
+    // their loads together and waits once, instead of one round trip per
+    // field as each is first used); divisions use the host's dividers.
+    const uint32_t bid = blockIdx.x;
+    uint32_t per_xcd = a.per_xcd, n_work = a.n_work, per_group = a.per_group, per_qt = a.per_qt;
+    uint32_t G = a.G, Hkv = a.Hkv, mode = a.mode, nqt = a.nqt, Lq = a.Lq, lens0 = a.lens_arg[0];
+    FastDiv fd_group = a.fd_group, fd_qt = a.fd_qt, fd_g = a.fd_g, fd_hkv = a.fd_hkv, fd_split = a.fd_split;
+    const uint16_t *qptr = a.q;
+    int64_t q_sb = a.q_sb, q_st = a.q_st, q_sh = a.q_sh;
+    asm volatile("" : "+s"(per_xcd), "+s"(n_work), "+s"(per_group), "+s"(per_qt), "+s"(G), "+s"(Hkv),
+                      "+s"(mode), "+s"(nqt), "+s"(Lq), "+s"(lens0), "+s"(fd_group.mul), "+s"(fd_group.shift),
+                      "+s"(fd_qt.mul), "+s"(fd_qt.shift), "+s"(fd_g.mul), "+s"(fd_g.shift), "+s"(fd_hkv.mul),
+                      "+s"(fd_hkv.shift), "+s"(fd_split.mul), "+s"(fd_split.shift), "+s"(qptr), "+s"(q_sb),
+                      "+s"(q_st), "+s"(q_sh));
+    const uint32_t w = (bid % NUM_XCD) * per_xcd + bid / NUM_XCD;
+    if (w >= n_work) return;
+    const uint32_t group = fastdiv(w, fd_group);
+    const uint32_t idx = w - group * per_group;
+    const uint32_t qi = fastdiv(idx, fd_qt);
+    const uint32_t rem = idx - qi * per_qt;
+    const uint32_t split = fastdiv(rem, fd_g);
+    const int hh = (int)(rem - split * G);
+    const int b = (int)fastdiv(group, fd_hkv);
+    const int kvh = (int)(group - b * Hkv);
+    const int hq = kvh * (int)G + hh;
+    const bool step = mode == MODE_STEP;
+    const int qt = step ? (int)qi : (int)(nqt - 1 - qi);  // prefill: heaviest tiles first
     const int q0 = qt * QT;
 
     const int tid = threadIdx.x;
@@ -192,11 +210,32 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     const int hf = lane >> 5;     // which half of the wave
     const int l32 = lane & 31;
 
+    // Query rows of this wave go global -> LDS -> registers, issued first
+    // thing: the direct loads stay in order with the tile loads, so one
+    // counted wait covers both.  They are staged in ring stages 2 and 3 (of
+    // the K ring for waves 0..3, of the V ring for waves 4..7), which are
+    // first refilled in loop step t_begin, after every wave has passed the
+    // prologue barrier.  The layout is that of a key tile, so the fragments
+    // are read like K.
+    static_assert(NB == 1, "query staging holds 32 rows per wave");
+    constexpr int QI = 32 * ROWB / 1024;   // wave-wide loads per wave
+    const uint32_t q_stage = (uint32_t)((wave < 4 ? 0 : VRING) + 2 * TILEB + (wave & 3) * 32 * ROWB);
+    {
+        const char *qg = (const char *)(qptr + b * q_sb + hq * q_sh);
+#pragma unroll
+        for (int i = 0; i < QI; ++i) {
+            const int r = i * RPW + lane / LPR;   // row within the wave's 32
+            const int ch = (lane % LPR) ^ swz<D>(r);
+            const int64_t t = min(q0 + wave * 32 + r, (int)Lq - 1);
+            dma16(qg + t * (2 * q_st) + 16 * ch, lds_addr(smem) + q_stage + i * 1024);
+        }
+    }
+
     // ---- key range ------------------------------------------------------
     const int32_t *offs = step ? nullptr : a.offsets + (int64_t)b * (a.nb + 1);
     int n_pool, k_hi, kfull;
     if (step) {
-        n_pool = (a.lens_in_args && b < LENS_IN_ARGS) ? a.lens_arg[b] : ld_uniform(a.cache_lens, b);
+        n_pool = !a.lens_in_args ? ld_uniform(a.cache_lens, b) : b == 0 ? (int)lens0 : a.lens_arg[b];
         k_hi = n_pool + a.Lq;
         kfull = k_hi;
     } else {
@@ -206,8 +245,9 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
         kfull = block_end<true>(offs, a.nb, q0);
     }
     const int ntile = (k_hi + KT - 1) / KT;
-    const int t_begin = (int)((int64_t)split * ntile / a.nsplit);
-    const int t_end = (int)((int64_t)(split + 1) * ntile / a.nsplit);
+    // (split * ntile < 2^31: ntile < 2^25 and split < WS_MAX_SPLITS)
+    const int t_begin = (int)fastdiv(split * (uint32_t)ntile, fd_split);
+    const int t_end = (int)fastdiv((split + 1) * (uint32_t)ntile, fd_split);
 
     // ---- page ids -------------------------------------------------------
     // The first three tiles' pages are read up front; the rest of the
@@ -225,7 +265,6 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     // ---- this lane's query rows -------------------------------------------
     // row n of the lane: q0 + wave * 32 * NB + 32 * n + l32 (the fragments
     // are staged through LDS in the pipeline prologue, below)
-    static_assert(NB == 1, "query staging holds 32 rows per wave");
     int row[NB], kend[NB];
     bf16x8 qf[NB][KK];
 #pragma unroll
@@ -361,25 +400,6 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
         vbase[e] = VRING + vr * ROWB + 16 * (vc ^ swz<D>(vr)) + 8 * (j16 & 1);
     }
 
-    // Query rows of this wave go global -> LDS -> registers: the direct
-    // loads stay in order with the tile loads, so one counted wait covers
-    // both and the first tile can be used while the second is in flight.
-    // They are staged in ring stages 2 and 3 (of the K ring for waves
-    // 0..3, of the V ring for waves 4..7), which are first refilled in loop
-    // step t_begin, after every wave has passed the prologue barrier.  The
-    // layout is that of a key tile, so the fragments are read like K.
-    constexpr int QI = 32 * ROWB / 1024;   // wave-wide loads per wave
-    const uint32_t q_stage = (uint32_t)((wave < 4 ? 0 : VRING) + 2 * TILEB + (wave & 3) * 32 * ROWB);
-    auto issue_q = [&]() {
-        const char *qg = (const char *)(a.q + b * a.q_sb + hq * a.q_sh);
-#pragma unroll
-        for (int i = 0; i < QI; ++i) {
-            const int r = i * RPW + lane / LPR;   // row within the wave's 32
-            const int ch = (lane % LPR) ^ swz<D>(r);
-            const int64_t t = min(q0 + wave * 32 + r, a.Lq - 1);
-            dma16(qg + t * (2 * a.q_st) + 16 * ch, lds_addr(smem) + q_stage + i * 1024);
-        }
-    };
     auto read_q = [&]() {
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk)
@@ -572,13 +592,12 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     const int n_tiles = t_end - t_begin;
     auto stage_off = [&](int t) -> uint32_t { return (uint32_t)((t - t_begin) % NSTAGE) * TILEB; };
     if (n_tiles > 0) {
-        // Prologue: every wave loads its query rows; the leading waves then
-        // issue the first two tiles and wait for the first (the second stays
-        // in flight into loop step t_begin, as in the steady state); the
-        // trailing waves stage the split's page ids in LDS.  The page-id
-        // reads are the only loads the compiler sees here, so its own waits
-        // never cover the tile loads.
-        issue_q();
+        // Prologue: the leading waves issue the first two tiles and wait for
+        // the first and their query rows (the second tile stays in flight
+        // into loop step t_begin, as in the steady state); the trailing waves
+        // stage the split's page ids in LDS.  The page-id reads are the only
+        // loads the compiler sees here, so its own waits never cover the
+        // tile loads.
         int pg_next = 0;   // page of tile j+2, read one step ahead
         if (lead) {
             const int pg0 = page_glb(t_begin), pg1 = page_glb(t_begin + 1);
@@ -628,6 +647,8 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
             wg_barrier();
         }
         if (lead) wg_barrier();
+    } else {
+        wait_vm_lgkm<0>();   // (the query loads)
     }
 
     // ---- epilogue -----------------------------------------------------------
