@@ -30,7 +30,7 @@ int ok() {
 }
 
 constexpr int NUM_CUS = 256;            // MI355X compute units
-constexpr int WS_MAX_SPLITS = 32;
+constexpr int WS_MAX_SPLITS = ws::MAX_SPLITS;
 constexpr int WS_MAX_HEAD_DIM = 128;
 
 int env_int(const char *name, int dflt) {

@@ -8,6 +8,8 @@ namespace ws {
 
 enum { MODE_PREFILL = 0, MODE_STEP = 1 };
 
+constexpr int MAX_SPLITS = 32;   // KV splits of one step at most
+
 // Division by a divisor d (1 <= d < 2^31) fixed for a launch, exact for
 // dividends n < 2^31: with l = ceil(log2 d), mul = ceil(2^(31+l) / d) and
 // shift = 31 + l, n / d = (n * mul) >> shift (the round-up method of

@@ -245,7 +245,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
         kfull = block_end<true>(offs, a.nb, q0);
     }
     const int ntile = (k_hi + KT - 1) / KT;
-    // (split * ntile < 2^31: ntile < 2^25 and split < WS_MAX_SPLITS)
+    // (split * ntile < 2^31: ntile < 2^25 and split < MAX_SPLITS = 32)
     const int t_begin = (int)fastdiv(split * (uint32_t)ntile, fd_split);
     const int t_end = (int)fastdiv((split + 1) * (uint32_t)ntile, fd_split);
 
@@ -769,21 +769,33 @@ __global__ __launch_bounds__(256) void combine16_kernel(const AttnArgs a) {
     const uint16_t *po = (const uint16_t *)a.part_o + blk * (32 * D) + pg * 512 + 8 * lane;
     const int64_t ls = nblk * 32;             // split stride of lse
     const int64_t ps = nblk * 32 * D;         // split stride of o
+    // all loads first (one round trip), then the arithmetic
+    float lse[MAX_SPLITS];
+    u32x4 ov[MAX_SPLITS];
+#pragma unroll
+    for (int s = 0; s < MAX_SPLITS; ++s) {
+        if (s < S) {
+            lse[s] = pl[s * ls];
+            ov[s] = *(const u32x4 *)(po + s * ps);
+        } else {
+            lse[s] = -INFINITY;
+            ov[s] = u32x4{0u, 0u, 0u, 0u};
+        }
+    }
     float M = -INFINITY;
-#pragma unroll 8
-    for (int s = 0; s < S; ++s) M = fmaxf(M, pl[s * ls]);
+#pragma unroll
+    for (int s = 0; s < MAX_SPLITS; ++s) M = fmaxf(M, lse[s]);
     const float Mu = (M == -INFINITY) ? 0.f : M;
     float L = 0.f;
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll 8
-    for (int s = 0; s < S; ++s) {
-        const float wgt = __builtin_amdgcn_exp2f(pl[s * ls] - Mu);
-        const u32x4 ov = *(const u32x4 *)(po + s * ps);
+#pragma unroll
+    for (int s = 0; s < MAX_SPLITS; ++s) {
+        const float wgt = __builtin_amdgcn_exp2f(lse[s] - Mu);   // 0 for absent splits
         L += wgt;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            acc[2 * k + 0] += __uint_as_float(ov[k] << 16) * wgt;
-            acc[2 * k + 1] += __uint_as_float(ov[k] & 0xFFFF0000u) * wgt;
+            acc[2 * k + 0] += __uint_as_float(ov[s][k] << 16) * wgt;
+            acc[2 * k + 1] += __uint_as_float(ov[s][k] & 0xFFFF0000u) * wgt;
         }
     }
     const float inv = L > 0.f ? 1.f / L : 0.f;
