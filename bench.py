@@ -166,6 +166,100 @@ def time_workload(wl, steps, warmup, dev, rotate=True):
     return wall_ms, float(per.mean()), float(np.median(per)), cases[0]
 
 
+# ---------------------------------------------------------------------------
+# KV-length sweeps: the step at growing cache lengths and small query blocks
+
+class SweepPoint:
+    """A streaming step of B streams (Hq query / Hkv KV heads x 128) with a
+    block of Lq new tokens against Lc cached tokens per stream, committed in
+    the same launch.  Inputs are N(0,1) bf16 drawn on the device from a
+    seeded generator (only their shape matters for timing); the pool pages
+    are a seeded random permutation, as in the headline workload."""
+
+    kind = "step"
+    D = 128
+    out_f32 = False
+    fuse_append = True
+
+    def __init__(self, sweep, B, Hq, Hkv, Lq, Lc):
+        self.sweep, self.B, self.Hq, self.Hkv, self.Lq, self.Lc = sweep, B, Hq, Hkv, Lq, Lc
+        self.cache_lens = np.full(B, Lc, dtype=np.int64)
+        self.name = f"{sweep}_b{B}_h{Hq}x{Hkv}_q{Lq}_c{Lc}"
+
+
+SWEEPS = ([SweepPoint("S1", 1, 24, 24, 256, c) for c in (0, 1024, 4096, 16384, 65536, 131072)]
+          + [SweepPoint("S2", 4, 64, 8, 512, c) for c in (4096, 16384, 32768, 65536, 131072)]
+          + [SweepPoint("S3", 4, 64, 8, lq, 131072) for lq in (16, 64)]
+          + [SweepPoint("S3", 1, 24, 24, lq, 131072) for lq in (16, 64)])
+
+
+class SweepCase:
+    def __init__(self, pt, dev, seed):
+        g = torch.Generator(device=dev)
+        g.manual_seed(seed)
+        B, Lq, Hq, Hkv, D = pt.B, pt.Lq, pt.Hq, pt.Hkv, pt.D
+        self.pt = pt
+        self.q = torch.randn((B, Lq, Hq, D), generator=g, device=dev).to(torch.bfloat16)
+        self.k_new = torch.randn((B, Lq, Hkv, D), generator=g, device=dev).to(torch.bfloat16)
+        self.v_new = torch.randn((B, Lq, Hkv, D), generator=g, device=dev).to(torch.bfloat16)
+        per = (pt.Lc + Lq + ws.PAGE_SIZE - 1) // ws.PAGE_SIZE
+        gh = torch.Generator()
+        gh.manual_seed(seed)
+        table = torch.randperm(B * per, generator=gh).to(torch.int32).reshape(B, per)
+        shape = (B * per, Hkv, ws.PAGE_SIZE, D)
+        kp = torch.randn(shape, generator=g, device=dev).to(torch.bfloat16)
+        vp = torch.randn(shape, generator=g, device=dev).to(torch.bfloat16)
+        self.cache = ws.PagedCache(kp, vp, table)
+        lens = torch.full((B,), pt.Lc, dtype=torch.int32)
+        self.lens = (lens, lens.to(dev))
+        self.out = torch.empty((B, Lq, Hq, D), dtype=torch.bfloat16, device=dev)
+        self.lse = torch.empty((B, Hq, Lq), dtype=torch.float32, device=dev)
+        need = ws.workspace_bytes(ws.WS_OP_STEP, B, Hq, Lq, pt.Lc + Lq)
+        self.workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+
+    def run(self):
+        ws.block_causal_attn_fwd(self.q, self.k_new, self.v_new, self.cache, self.lens,
+                                 fuse_append=True, out=self.out, lse=self.lse, want_lse=True,
+                                 workspace=self.workspace)
+
+
+def run_sweeps(dev, steps):
+    """Median HIP-event time per point, over device copies rotated so that
+    more than the 256 MB last-level cache is touched between reuses."""
+    points = []
+    for i, pt in enumerate(SWEEPS):
+        nbytes = algorithmic_bytes(pt)
+        copies = min(64, max(1, math.ceil(ROTATE_BYTES / nbytes)))
+        cases = [SweepCase(pt, dev, 7000 + 100 * i + c) for c in range(copies)]
+        torch.cuda.synchronize()
+        n = max(5, min(steps, int(2e5 / max(1.0, nbytes / 1e6))))   # ~ a fixed byte budget per point
+        for c in range(min(3, n)):
+            cases[c % copies].run()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        for k in range(n):
+            ev[k][0].record()
+            cases[k % copies].run()
+            ev[k][1].record()
+        torch.cuda.synchronize()
+        ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+        flops = algorithmic_flops(pt)
+        tf = flops / (ms * 1e-3) / 1e12
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        ai = flops / nbytes
+        attain = min(BF16_PEAK_TFLOPS, ai * HBM_PEAK_GBS / 1e3)
+        points.append({"sweep": pt.sweep, "workload": pt.name, "batch": pt.B, "q_heads": pt.Hq,
+                       "kv_heads": pt.Hkv, "block_tokens": pt.Lq, "cache_tokens": pt.Lc,
+                       "ms": round(ms, 5), "TFLOP/s": round(tf, 1), "GB/s": round(gbs, 1),
+                       "flop_per_byte": round(ai, 1),
+                       "bound": "hbm" if ai * HBM_PEAK_GBS / 1e3 < BF16_PEAK_TFLOPS else "mfma",
+                       "frac_of_bound": round(tf / attain, 4),
+                       "mfma_frac": round(tf / BF16_PEAK_TFLOPS, 4), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)})
+        log(f"[bench] sweep {pt.name}: {ms * 1e3:.1f} us, {tf:.0f} TFLOP/s, {gbs:.0f} GB/s")
+        del cases
+        torch.cuda.empty_cache()
+    return points
+
+
 def cpu_baseline(wl):
     """The fp64 oracle (as it stands) on the whole headline step."""
     import oracle  # test infrastructure: only this baseline leg uses it
@@ -203,6 +297,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-extra", action="store_true", help="headline workload only")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the KV-length sweeps")
     ap.add_argument("--config", type=int, default=2, help="headline workload index (1-5)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (to calibrate "
@@ -264,6 +359,7 @@ def main():
             del w2
             torch.cuda.empty_cache()
 
+    sweeps = [] if (args.no_extra or args.no_sweep) else run_sweeps(dev, 200)
     cpu = None if args.no_cpu else cpu_baseline(wl)
     line = {
         "metric": METRIC,
@@ -287,6 +383,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "extra": extra,
+        "sweeps": sweeps,
         "gpu": torch.cuda.get_device_name(0),
     }
     print(json.dumps(line), flush=True)
