@@ -109,7 +109,7 @@ class DeviceCase:
             zero = torch.zeros(wl.B, dtype=torch.int32)
             ws.kv_append(self.cache, (zero, zero.to(dev)), kc[:, :n], vc[:, :n])
             del kc, vc
-            need = ws.workspace_bytes(ws.WS_OP_STEP, wl.B, wl.Hq, wl.Lq,
+            need = ws.workspace_bytes(ws.WS_OP_STEP, wl.B, wl.Hq, wl.Hkv, wl.Lq,
                                       int(wl.cache_lens.max()) + wl.Lq)
             self.workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
         else:
@@ -214,7 +214,7 @@ class SweepCase:
         self.lens = (lens, lens.to(dev))
         self.out = torch.empty((B, Lq, Hq, D), dtype=torch.bfloat16, device=dev)
         self.lse = torch.empty((B, Hq, Lq), dtype=torch.float32, device=dev)
-        need = ws.workspace_bytes(ws.WS_OP_STEP, B, Hq, Lq, pt.Lc + Lq)
+        need = ws.workspace_bytes(ws.WS_OP_STEP, B, Hq, Hkv, Lq, pt.Lc + Lq)
         self.workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
 
     def run(self):

@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define WS_ABI_VERSION 1
+#define WS_ABI_VERSION 2
 #define WS_PAGE_SIZE 64
 
 typedef enum {
@@ -159,9 +159,11 @@ int ws_kv_append(const ws_paged_kv *kv, int32_t batch,
  *   out:         bf16 or f32 [batch][new_len][num_q_heads][head_dim]
  *   lse:         NULL or device f32 [batch][num_q_heads][new_len]
  *   workspace:   device scratch of at least
- *                ws_workspace_bytes(WS_OP_STEP, batch, num_q_heads, new_len,
- *                max_b cache_lens[b] + new_len) bytes (NULL allowed when
- *                that is 0); its contents on entry are ignored.
+ *                ws_workspace_bytes(WS_OP_STEP, batch, num_q_heads,
+ *                kv->num_kv_heads, new_len, max_b cache_lens[b] + new_len)
+ *                bytes (NULL allowed when that is 0); its contents on entry
+ *                are ignored.
+ * new_len x (num_q_heads / num_kv_heads) must not exceed 2^30 (WS_ERR_SHAPE).
  * Errors: WS_ERR_NULL, WS_ERR_SHAPE, WS_ERR_UNSUPPORTED, WS_ERR_ALIGN,
  * WS_ERR_HEADS, WS_ERR_CAPACITY, WS_ERR_PAGE, WS_ERR_WORKSPACE, WS_ERR_HIP.
  */
@@ -201,10 +203,11 @@ int ws_block_causal_prefill(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v,
 
 /*
  * Workspace bytes ws_block_causal_attn_fwd needs for this shape (op =
- * WS_OP_STEP; max_k = largest cache_lens[b] + new_len).  WS_OP_PREFILL
- * returns 0.  Pure host arithmetic; returns 0 for invalid arguments.
+ * WS_OP_STEP; num_kv_heads = the cache's; max_k = largest cache_lens[b] +
+ * new_len).  WS_OP_PREFILL returns 0.  Pure host arithmetic; returns 0 for
+ * invalid arguments.
  */
-size_t ws_workspace_bytes(int32_t op, int32_t batch, int32_t num_q_heads,
+size_t ws_workspace_bytes(int32_t op, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
                           int32_t max_q, int32_t max_k);
 
 #ifdef __cplusplus

@@ -9,7 +9,7 @@ Entry points (same names as the C ABI, without the ``ws_`` prefix):
   kv_append(cache, cache_lens, k_new, v_new)
   block_causal_attn_fwd(q, k_new, v_new, cache, cache_lens, ...)
   block_causal_prefill(q, k, v, block_offsets, ...)
-  workspace_bytes(op, batch, num_q_heads, max_q, max_k)
+  workspace_bytes(op, batch, num_q_heads, num_kv_heads, max_q, max_k)
 """
 import ctypes
 import math
@@ -69,7 +69,7 @@ def library():
         lib.ws_status_string.argtypes = [ctypes.c_int]
         lib.ws_last_error.restype = ctypes.c_char_p
         lib.ws_workspace_bytes.restype = ctypes.c_size_t
-        lib.ws_workspace_bytes.argtypes = [I32, I32, I32, I32, I32]
+        lib.ws_workspace_bytes.argtypes = [I32, I32, I32, I32, I32, I32]
         lib.ws_kv_append.restype = ctypes.c_int
         lib.ws_kv_append.argtypes = [ctypes.POINTER(PagedKVDesc), I32, P, P, I32, Tensor4, Tensor4, P]
         lib.ws_block_causal_attn_fwd.restype = ctypes.c_int
@@ -80,7 +80,7 @@ def library():
         lib.ws_block_causal_prefill.argtypes = [
             Tensor4, Tensor4, Tensor4, ctypes.POINTER(PagedKVDesc), P, P, I32, I32, I32, I32, I32,
             I32, F, Tensor4, P, P]
-        if lib.ws_abi_version() != 1:
+        if lib.ws_abi_version() != 2:
             raise RuntimeError("libwsattn.so ABI version mismatch")
         _LIB = lib
     return _LIB
@@ -180,8 +180,8 @@ def _check_table(cache, B):
         raise ValueError("page table has fewer rows than the batch")
 
 
-def workspace_bytes(op, batch, num_q_heads, max_q, max_k):
-    return library().ws_workspace_bytes(op, batch, num_q_heads, max_q, max_k)
+def workspace_bytes(op, batch, num_q_heads, num_kv_heads, max_q, max_k):
+    return library().ws_workspace_bytes(op, batch, num_q_heads, num_kv_heads, max_q, max_k)
 
 
 def kv_append(cache, cache_lens, k_new, v_new):
@@ -220,7 +220,7 @@ def block_causal_attn_fwd(q, k_new, v_new, cache, cache_lens, scale=None, fuse_a
     _check_lens(host, dev, B)
     _check_table(cache, B)
     max_k = int(host.max().item()) + Lq if B > 0 else Lq
-    need = workspace_bytes(WS_OP_STEP, B, Hq, Lq, max_k) if B > 0 and Lq > 0 else 0
+    need = workspace_bytes(WS_OP_STEP, B, Hq, cache.num_kv_heads, Lq, max_k) if B > 0 and Lq > 0 else 0
     if workspace is None and need > 0:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
     ws_ptr = _ptr(workspace)

@@ -31,6 +31,9 @@ int ok() {
 
 constexpr int NUM_CUS = 256;            // MI355X compute units
 constexpr int WS_MAX_SPLITS = ws::MAX_SPLITS;
+// packed query rows of one (stream, KV head) in a step: G x new_len (the
+// kernels index them in 32-bit arithmetic)
+constexpr int64_t WS_MAX_STEP_ROWS = ((int64_t)1 << 30);
 constexpr int WS_MAX_HEAD_DIM = 128;
 
 int env_int(const char *name, int dflt) {
@@ -112,12 +115,15 @@ struct StepPlan {
 // One launch shape: 8 waves x 32 query rows (256-query tiles).
 ws::TileShape default_shape() { return ws::TileShape{1, 8}; }
 
-StepPlan plan_step(int batch, int hq, int lq, int64_t max_k) {
+// The step packs the G query heads of a KV group into one row space of
+// G * lq rows (see AttnArgs).
+StepPlan plan_step(int batch, int hq, int hkv, int lq, int64_t max_k) {
     StepPlan p;
     p.shape = default_shape();
-    const int qt = p.shape.qtile();
-    p.nqt = (lq + qt - 1) / qt;
-    const int64_t base = (int64_t)batch * hq * p.nqt;
+    const int64_t qt = p.shape.qtile();
+    const int64_t rows = (int64_t)(hq / hkv) * lq;
+    p.nqt = (int)((rows + qt - 1) / qt);
+    const int64_t base = (int64_t)batch * hkv * p.nqt;
     const int64_t ntiles = (max_k + 63) / 64;
     const int64_t slots = (int64_t)NUM_CUS * p.shape.groups_per_cu();
     int64_t ns = 1;
@@ -132,26 +138,27 @@ StepPlan plan_step(int batch, int hq, int lq, int64_t max_k) {
     return p;
 }
 
-// Partials are kept in blocks of 32 query rows.
-size_t step_workspace(const StepPlan &p, int batch, int hq, int lq) {
+// Partials are kept in blocks of 32 packed rows per (stream, KV head).
+size_t step_workspace(const StepPlan &p, int batch, int hq, int hkv, int lq) {
     if (p.nsplit <= 1) return 0;
-    const size_t rows = (size_t)(lq + 31) / 32 * 32;
-    return (size_t)p.nsplit * batch * hq * rows * (WS_MAX_HEAD_DIM + 2) * sizeof(float);
+    const size_t rows = ((size_t)(hq / hkv) * lq + 31) / 32 * 32;
+    return (size_t)p.nsplit * batch * hkv * rows * (WS_MAX_HEAD_DIM + 2) * sizeof(float);
 }
 
 ws::TileShape plan_prefill(int) { return default_shape(); }
 
 // Total work items; fails when the grid would not fit the kernel's int math.
 bool finish_work(ws::AttnArgs &a) {
-    const int64_t n = (int64_t)a.B * a.Hq * a.nqt * a.nsplit;
+    const int64_t n = (int64_t)a.B * a.Hkv * a.gi * a.nqt * a.nsplit;
     if (n > (int64_t)1 << 30) return false;
     a.n_work = (int32_t)n;
     a.per_xcd = (a.n_work + 7) / 8;
-    a.per_qt = a.G * a.nsplit;
+    a.per_qt = a.gi * a.nsplit;
     a.per_group = a.per_qt * a.nqt;
     a.fd_group = ws::fastdiv_make((uint32_t)a.per_group);
     a.fd_qt = ws::fastdiv_make((uint32_t)a.per_qt);
-    a.fd_g = ws::fastdiv_make((uint32_t)a.G);
+    a.fd_g = ws::fastdiv_make((uint32_t)a.gi);
+    a.fd_gq = ws::fastdiv_make((uint32_t)a.G);
     a.fd_hkv = ws::fastdiv_make((uint32_t)a.Hkv);
     a.fd_split = ws::fastdiv_make((uint32_t)a.nsplit);
     return true;
@@ -182,11 +189,15 @@ const char *ws_status_string(int status) {
 
 const char *ws_last_error(void) { return g_err; }
 
-size_t ws_workspace_bytes(int32_t op, int32_t batch, int32_t num_q_heads, int32_t max_q, int32_t max_k) {
+size_t ws_workspace_bytes(int32_t op, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                          int32_t max_q, int32_t max_k) {
     if (op != WS_OP_STEP) return 0;
-    if (batch <= 0 || num_q_heads <= 0 || max_q <= 0 || max_k < max_q) return 0;
-    const StepPlan p = plan_step(batch, num_q_heads, max_q, max_k);
-    return step_workspace(p, batch, num_q_heads, max_q);
+    if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads || max_q <= 0 ||
+        max_k < max_q)
+        return 0;
+    if ((int64_t)(num_q_heads / num_kv_heads) * max_q > WS_MAX_STEP_ROWS) return 0;
+    const StepPlan p = plan_step(batch, num_q_heads, num_kv_heads, max_q, max_k);
+    return step_workspace(p, batch, num_q_heads, num_kv_heads, max_q);
 }
 
 int ws_kv_append(const ws_paged_kv *kv, int32_t batch, const int32_t *cache_lens_host,
@@ -246,8 +257,10 @@ int ws_block_causal_attn_fwd(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, c
         if ((int64_t)cache_lens_host[b] + new_len > max_k) max_k = (int64_t)cache_lens_host[b] + new_len;
     }
     if (max_k > INT32_MAX) return fail(WS_ERR_SHAPE, "too many keys");
-    const StepPlan plan = plan_step(batch, num_q_heads, new_len, max_k);
-    const size_t need_ws = step_workspace(plan, batch, num_q_heads, new_len);
+    if ((int64_t)(num_q_heads / kv->num_kv_heads) * new_len > WS_MAX_STEP_ROWS)
+        return fail(WS_ERR_SHAPE, "new_len x query heads per KV head exceeds %lld", (long long)WS_MAX_STEP_ROWS);
+    const StepPlan plan = plan_step(batch, num_q_heads, kv->num_kv_heads, new_len, max_k);
+    const size_t need_ws = step_workspace(plan, batch, num_q_heads, kv->num_kv_heads, new_len);
     if (need_ws > 0 && (!workspace || workspace_bytes < need_ws || !aligned16(workspace)))
         return fail(WS_ERR_WORKSPACE, "workspace needs %zu bytes (16-byte aligned), got %zu", need_ws,
                     workspace ? workspace_bytes : (size_t)0);
@@ -268,10 +281,12 @@ int ws_block_causal_attn_fwd(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, c
     a.nsplit = plan.nsplit;
     a.nqt = plan.nqt;
     a.scale_log2 = scale * 1.4426950408889634f;
-    a.nrb = (new_len + 31) / 32;
+    a.gi = 1;
+    a.nrows = a.G * new_len;
+    a.nrb = (a.nrows + 31) / 32;
     if (plan.nsplit > 1) {
         a.part_o = (float *)workspace;
-        a.part_ml = a.part_o + (size_t)plan.nsplit * batch * num_q_heads * a.nrb * 32 * kv->head_dim;
+        a.part_ml = a.part_o + (size_t)plan.nsplit * batch * a.Hkv * a.nrb * 32 * kv->head_dim;
     }
     if (batch <= ws::LENS_IN_ARGS) {
         a.lens_in_args = 1;
@@ -347,6 +362,8 @@ int ws_block_causal_prefill(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, const ws_p
     a.B = batch; a.Lq = seq_len; a.Hq = num_q_heads; a.Hkv = num_kv_heads; a.G = num_q_heads / num_kv_heads;
     a.mode = ws::MODE_PREFILL;
     a.nsplit = 1;
+    a.gi = a.G;
+    a.nrows = seq_len;
     a.nqt = (seq_len + shape.qtile() - 1) / shape.qtile();
     a.scale_log2 = scale * 1.4426950408889634f;
     if (!finish_work(a)) return fail(WS_ERR_SHAPE, "too many work items");

@@ -55,14 +55,20 @@ struct AttnArgs {
     int64_t o_sb, o_st, o_sh;
     int32_t out_f32;
     float *lse;
-    // split-KV partials, in blocks of 32 query rows (nrb = ceil(Lq / 32)
-    // blocks per (b, hq)).  f32 output: o [S][B][Hq][nrb][D/4][64 lanes][4]
+    // Query rows.  Prefill: one work item per query head, rows are tokens.
+    // Step: the G query heads of a KV group are packed into one row space,
+    // row p = t * G + hh for token t and head kvh * G + hh, so small blocks
+    // still fill the query tiles; nrows = G * Lq rows per (b, KV head).
+    // split-KV partials (step only), in blocks of 32 packed rows (nrb =
+    // ceil(G * Lq / 32) blocks per (b, KV head)).  f32 output: o [S][B][Hq][nrb][D/4][64 lanes][4]
     // f32 unnormalised, in the accumulator's register order, and (m, l)
     // [S][B][Hq][nrb * 32][2].  bf16 output: o / l as bf16
     // [S][B][Hq][nrb][D/8][64 lanes][8] in register order (two accumulator
     // groups per lane) and m + log2(l) [S][B][Hq][nrb * 32] f32 at part_ml.
     float *part_o, *part_ml;
     int32_t nrb;
+    int32_t nrows;       // rows per item's head space: Lq (prefill) or G * Lq (step)
+    int32_t gi;          // work items per (b, KV head, q-tile, split): G (prefill) or 1 (step)
     int32_t B, Lq, Hq, Hkv, G;
     int32_t mode;        // MODE_PREFILL or MODE_STEP
     int32_t paged;       // prefill only: keys/values come from the pool
@@ -75,6 +81,7 @@ struct AttnArgs {
     int32_t per_qt;      // G * nsplit: work items per (b, KV head, q-tile)
     // dividers by per_group, per_qt, G, Hkv and nsplit
     FastDiv fd_group, fd_qt, fd_g, fd_hkv, fd_split;
+    FastDiv fd_gq;       // divider by G (packed row -> token)
     float scale_log2;    // scale * log2(e)
     // step: cache lengths also passed by value when batch <= LENS_IN_ARGS,
     // so the first page lookup does not wait on a load of them

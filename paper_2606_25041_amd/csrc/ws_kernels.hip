@@ -180,15 +180,16 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     // field as each is first used); divisions use the host's dividers.
     const uint32_t bid = blockIdx.x;
     uint32_t per_xcd = a.per_xcd, n_work = a.n_work, per_group = a.per_group, per_qt = a.per_qt;
-    uint32_t G = a.G, Hkv = a.Hkv, mode = a.mode, nqt = a.nqt, Lq = a.Lq, lens0 = a.lens_arg[0];
+    uint32_t G = a.G, gi = a.gi, Hkv = a.Hkv, mode = a.mode, nqt = a.nqt, nrows = a.nrows, lens0 = a.lens_arg[0];
     FastDiv fd_group = a.fd_group, fd_qt = a.fd_qt, fd_g = a.fd_g, fd_hkv = a.fd_hkv, fd_split = a.fd_split;
+    FastDiv fd_gq = a.fd_gq;
     const uint16_t *qptr = a.q;
     int64_t q_sb = a.q_sb, q_st = a.q_st, q_sh = a.q_sh;
-    asm volatile("" : "+s"(per_xcd), "+s"(n_work), "+s"(per_group), "+s"(per_qt), "+s"(G), "+s"(Hkv),
-                      "+s"(mode), "+s"(nqt), "+s"(Lq), "+s"(lens0), "+s"(fd_group.mul), "+s"(fd_group.shift),
+    asm volatile("" : "+s"(per_xcd), "+s"(n_work), "+s"(per_group), "+s"(per_qt), "+s"(G), "+s"(gi), "+s"(Hkv),
+                      "+s"(mode), "+s"(nqt), "+s"(nrows), "+s"(lens0), "+s"(fd_group.mul), "+s"(fd_group.shift),
                       "+s"(fd_qt.mul), "+s"(fd_qt.shift), "+s"(fd_g.mul), "+s"(fd_g.shift), "+s"(fd_hkv.mul),
-                      "+s"(fd_hkv.shift), "+s"(fd_split.mul), "+s"(fd_split.shift), "+s"(qptr), "+s"(q_sb),
-                      "+s"(q_st), "+s"(q_sh));
+                      "+s"(fd_hkv.shift), "+s"(fd_split.mul), "+s"(fd_split.shift), "+s"(fd_gq.mul),
+                      "+s"(fd_gq.shift), "+s"(qptr), "+s"(q_sb), "+s"(q_st), "+s"(q_sh));
     const uint32_t w = (bid % NUM_XCD) * per_xcd + bid / NUM_XCD;
     if (w >= n_work) return;
     const uint32_t group = fastdiv(w, fd_group);
@@ -196,11 +197,14 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     const uint32_t qi = fastdiv(idx, fd_qt);
     const uint32_t rem = idx - qi * per_qt;
     const uint32_t split = fastdiv(rem, fd_g);
-    const int hh = (int)(rem - split * G);
+    const int hh = (int)(rem - split * gi);
     const int b = (int)fastdiv(group, fd_hkv);
     const int kvh = (int)(group - b * Hkv);
-    const int hq = kvh * (int)G + hh;
+    const int hq = kvh * (int)G + hh;   // (prefill; a step's rows span the group's heads)
     const bool step = mode == MODE_STEP;
+    // token and query head of packed row p (see AttnArgs)
+    auto row_token = [&](int p) -> int { return step ? (int)fastdiv((uint32_t)p, fd_gq) : p; };
+    auto row_head = [&](int p, int t) -> int { return step ? kvh * (int)G + (p - t * (int)G) : hq; };
     const int qt = step ? (int)qi : (int)(nqt - 1 - qi);  // prefill: heaviest tiles first
     const int q0 = qt * QT;
 
@@ -221,13 +225,15 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     constexpr int QI = 32 * ROWB / 1024;   // wave-wide loads per wave
     const uint32_t q_stage = (uint32_t)((wave < 4 ? 0 : VRING) + 2 * TILEB + (wave & 3) * 32 * ROWB);
     {
-        const char *qg = (const char *)(qptr + b * q_sb + hq * q_sh);
+        const char *qg = (const char *)(qptr + b * q_sb);
 #pragma unroll
         for (int i = 0; i < QI; ++i) {
             const int r = i * RPW + lane / LPR;   // row within the wave's 32
             const int ch = (lane % LPR) ^ swz<D>(r);
-            const int64_t t = min(q0 + wave * 32 + r, (int)Lq - 1);
-            dma16(qg + t * (2 * q_st) + 16 * ch, lds_addr(smem) + q_stage + i * 1024);
+            const int p = min(q0 + wave * 32 + r, (int)nrows - 1);
+            const int t = row_token(p);
+            const int h = row_head(p, t);
+            dma16(qg + (int64_t)t * (2 * q_st) + (int64_t)h * (2 * q_sh) + 16 * ch, lds_addr(smem) + q_stage + i * 1024);
         }
     }
 
@@ -265,12 +271,15 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     // ---- this lane's query rows -------------------------------------------
     // row n of the lane: q0 + wave * 32 * NB + 32 * n + l32 (the fragments
     // are staged through LDS in the pipeline prologue, below)
-    int row[NB], kend[NB];
+    int row[NB], kend[NB], tok[NB], hqr[NB];
     bf16x8 qf[NB][KK];
 #pragma unroll
     for (int n = 0; n < NB; ++n) {
         row[n] = q0 + wave * 32 * NB + 32 * n + l32;
-        kend[n] = step ? k_hi : block_end<false>(offs, a.nb, min(row[n], a.Lq - 1));
+        const int pc = min(row[n], (int)nrows - 1);
+        tok[n] = row_token(pc);
+        hqr[n] = row_head(pc, tok[n]);
+        kend[n] = step ? k_hi : block_end<false>(offs, a.nb, tok[n]);
     }
 
     // ---- direct-to-LDS tile loads -----------------------------------------
@@ -656,11 +665,12 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     for (int n = 0; n < NB; ++n) {
         const float lt = halves_sum(l[n]);
         const int r = row[n];
-        if (r >= a.Lq) continue;
+        if (r >= (int)nrows) continue;
+        const int t = tok[n], h = hqr[n];
         if (a.nsplit == 1) {
             const float inv = lt > 0.f ? 1.f / lt : 0.f;
             if (a.out_f32) {
-                float *op = (float *)a.out + b * a.o_sb + (int64_t)r * a.o_st + hq * a.o_sh;
+                float *op = (float *)a.out + b * a.o_sb + (int64_t)t * a.o_st + h * a.o_sh;
 #pragma unroll
                 for (int md = 0; md < MD; ++md)
 #pragma unroll
@@ -671,7 +681,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
                         *(f32x4 *)(op + 32 * md + 8 * g + 4 * hf) = val;
                     }
             } else {
-                uint16_t *op = (uint16_t *)a.out + b * a.o_sb + (int64_t)r * a.o_st + hq * a.o_sh;
+                uint16_t *op = (uint16_t *)a.out + b * a.o_sb + (int64_t)t * a.o_st + h * a.o_sh;
 #pragma unroll
                 for (int md = 0; md < MD; ++md)
 #pragma unroll
@@ -683,12 +693,12 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
                     }
             }
             if (a.lse && hf == 0)
-                a.lse[((int64_t)b * a.Hq + hq) * a.Lq + r] = (m[n] + __builtin_amdgcn_logf(lt)) * 0.69314718055994531f;
+                a.lse[((int64_t)b * a.Hq + h) * a.Lq + t] = (m[n] + __builtin_amdgcn_logf(lt)) * 0.69314718055994531f;
         } else if (!a.out_f32) {
             // bf16 output: o / l rounded to bf16 and the split's log2-domain
             // lse; register order, two accumulator groups (16 bytes) per
             // lane, so each store instruction writes 1 KB contiguous
-            const int64_t blk = (((int64_t)split * a.B + b) * a.Hq + hq) * a.nrb + (r >> 5);
+            const int64_t blk = (((int64_t)split * a.B + b) * a.Hkv + kvh) * a.nrb + (r >> 5);
             const float inv = lt > 0.f ? 1.f / lt : 0.f;
             uint16_t *op = (uint16_t *)a.part_o + blk * (32 * D) + 8 * lane;
 #pragma unroll
@@ -705,7 +715,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
             if (hf == 0) a.part_ml[blk * 32 + l32] = lt > 0.f ? m[n] + __builtin_amdgcn_logf(lt) : -INFINITY;
         } else {
             // register order: each store instruction writes 1 KB contiguous
-            const int64_t blk = (((int64_t)split * a.B + b) * a.Hq + hq) * a.nrb + (r >> 5);
+            const int64_t blk = (((int64_t)split * a.B + b) * a.Hkv + kvh) * a.nrb + (r >> 5);
             float *op = a.part_o + blk * (32 * D) + 4 * lane;
 #pragma unroll
             for (int md = 0; md < MD; ++md)
@@ -724,8 +734,9 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     }
 
     // ---- fused append -----------------------------------------------------
-    // The G query heads of a group share one KV head, so only the items of
-    // its first head write; they split the new tokens evenly among them.
+    // Step items cover every query head of their KV group (packed rows),
+    // so the items of a (stream, KV head) group split the new tokens evenly
+    // among them.
     // This kernel reads the new block from kc/vc, never from the slots being
     // written, so the append can trail the attention; it comes after the
     // epilogue's stores so that its loads overlap their drain.
@@ -753,17 +764,19 @@ template <int D>
 __global__ __launch_bounds__(256) void combine16_kernel(const AttnArgs a) {
     constexpr int MD = D / 32;
     constexpr int PER_BLK = 2 * MD * 64;      // 16-byte items per 32-row block
-    const int64_t nblk = (int64_t)a.B * a.Hq * a.nrb;
+    const int64_t nblk = (int64_t)a.B * a.Hkv * a.nrb;
     const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (u >= nblk * PER_BLK) return;
     const int64_t blk = u / PER_BLK;
     const int item = (int)(u % PER_BLK);
     const int lane = item & 63;
     const int pg = item >> 6;                 // md * 2 + g0 / 2
-    const int r = (int)(blk % a.nrb) * 32 + (lane & 31);
-    if (r >= a.Lq) return;
-    const int hq = (int)((blk / a.nrb) % a.Hq);
-    const int b = (int)(blk / ((int64_t)a.nrb * a.Hq));
+    const int r = (int)(blk % a.nrb) * 32 + (lane & 31);   // packed row
+    if (r >= a.nrows) return;
+    const int kvh = (int)((blk / a.nrb) % a.Hkv);
+    const int b = (int)(blk / ((int64_t)a.nrb * a.Hkv));
+    const int t = r / a.G;
+    const int hq = kvh * a.G + (r - t * a.G);
     const int S = a.nsplit;
     const float *pl = a.part_ml + blk * 32 + (lane & 31);
     const uint16_t *po = (const uint16_t *)a.part_o + blk * (32 * D) + pg * 512 + 8 * lane;
@@ -800,7 +813,7 @@ __global__ __launch_bounds__(256) void combine16_kernel(const AttnArgs a) {
     }
     const float inv = L > 0.f ? 1.f / L : 0.f;
     const int md = pg >> 1, g0 = 2 * (pg & 1), hf = lane >> 5;
-    uint16_t *op = (uint16_t *)a.out + b * a.o_sb + (int64_t)r * a.o_st + hq * a.o_sh + 32 * md + 4 * hf;
+    uint16_t *op = (uint16_t *)a.out + b * a.o_sb + (int64_t)t * a.o_st + hq * a.o_sh + 32 * md + 4 * hf;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
         u32x2 val;
@@ -809,7 +822,7 @@ __global__ __launch_bounds__(256) void combine16_kernel(const AttnArgs a) {
         *(u32x2 *)(op + 8 * (g0 + h)) = val;
     }
     if (a.lse && pg == 0 && lane < 32)
-        a.lse[((int64_t)b * a.Hq + hq) * a.Lq + r] = (M + __builtin_amdgcn_logf(L)) * 0.69314718055994531f;
+        a.lse[((int64_t)b * a.Hq + hq) * a.Lq + t] = (M + __builtin_amdgcn_logf(L)) * 0.69314718055994531f;
 }
 
 // Merge the KV-split partials of every query row: with per-split running
@@ -823,17 +836,19 @@ template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(const AttnArgs a) {
     constexpr int MD = D / 32;
     constexpr int PER_BLK = MD * 4 * 64;      // float4 items per 32-row block
-    const int64_t nblk = (int64_t)a.B * a.Hq * a.nrb;
+    const int64_t nblk = (int64_t)a.B * a.Hkv * a.nrb;
     const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (u >= nblk * PER_BLK) return;
     const int64_t blk = u / PER_BLK;
     const int item = (int)(u % PER_BLK);
     const int lane = item & 63;
     const int mg = item >> 6;                 // md * 4 + g
-    const int r = (int)(blk % a.nrb) * 32 + (lane & 31);
-    if (r >= a.Lq) return;
-    const int hq = (int)((blk / a.nrb) % a.Hq);
-    const int b = (int)(blk / ((int64_t)a.nrb * a.Hq));
+    const int r = (int)(blk % a.nrb) * 32 + (lane & 31);   // packed row
+    if (r >= a.nrows) return;
+    const int kvh = (int)((blk / a.nrb) % a.Hkv);
+    const int b = (int)(blk / ((int64_t)a.nrb * a.Hkv));
+    const int t = r / a.G;
+    const int hq = kvh * a.G + (r - t * a.G);
     const int d0 = 32 * (mg >> 2) + 8 * (mg & 3) + 4 * (lane >> 5);
     const int S = a.nsplit;
     const float2 *ml = (const float2 *)a.part_ml + blk * 32 + (lane & 31);
@@ -857,20 +872,20 @@ __global__ __launch_bounds__(256) void combine_kernel(const AttnArgs a) {
     }
     const float inv = L > 0.f ? 1.f / L : 0.f;
     if (a.out_f32) {
-        float *op = (float *)a.out + b * a.o_sb + (int64_t)r * a.o_st + hq * a.o_sh + d0;
+        float *op = (float *)a.out + b * a.o_sb + (int64_t)t * a.o_st + hq * a.o_sh + d0;
         f32x4 val;
 #pragma unroll
         for (int e = 0; e < 4; ++e) val[e] = acc[e] * inv;
         *(f32x4 *)op = val;
     } else {
-        uint16_t *op = (uint16_t *)a.out + b * a.o_sb + (int64_t)r * a.o_st + hq * a.o_sh + d0;
+        uint16_t *op = (uint16_t *)a.out + b * a.o_sb + (int64_t)t * a.o_st + hq * a.o_sh + d0;
         u32x2 val;
         val[0] = pack_bf16x2(acc[0] * inv, acc[1] * inv);
         val[1] = pack_bf16x2(acc[2] * inv, acc[3] * inv);
         *(u32x2 *)op = val;
     }
     if (a.lse && mg == 0 && lane < 32)
-        a.lse[((int64_t)b * a.Hq + hq) * a.Lq + r] = (M + __builtin_amdgcn_logf(L)) * 0.69314718055994531f;
+        a.lse[((int64_t)b * a.Hq + hq) * a.Lq + t] = (M + __builtin_amdgcn_logf(L)) * 0.69314718055994531f;
 }
 
 // Copy new tokens' K/V rows into their cache slots: one 16-byte chunk per
@@ -912,7 +927,7 @@ int launch_attention(const AttnArgs &a, int head_dim, TileShape shape, void *str
 int launch_combine(const AttnArgs &a, int head_dim, void *stream) {
     hipStream_t st = (hipStream_t)stream;
     if (!a.out_f32) {
-        const int64_t items = (int64_t)a.B * a.Hq * a.nrb * (head_dim / 32) * 2 * 64;
+        const int64_t items = (int64_t)a.B * a.Hkv * a.nrb * (head_dim / 32) * 2 * 64;
         const int64_t grid = (items + 255) / 256;
         if (head_dim == 128)
             hipLaunchKernelGGL(combine16_kernel<128>, dim3((unsigned)grid), dim3(256), 0, st, a);
@@ -920,7 +935,7 @@ int launch_combine(const AttnArgs &a, int head_dim, void *stream) {
             hipLaunchKernelGGL(combine16_kernel<64>, dim3((unsigned)grid), dim3(256), 0, st, a);
         return (int)hipGetLastError();
     }
-    const int64_t items = (int64_t)a.B * a.Hq * a.nrb * (head_dim / 32) * 4 * 64;
+    const int64_t items = (int64_t)a.B * a.Hkv * a.nrb * (head_dim / 32) * 4 * 64;
     const int64_t grid = (items + 255) / 256;
     if (head_dim == 128)
         hipLaunchKernelGGL(combine_kernel<128>, dim3((unsigned)grid), dim3(256), 0, st, a);

@@ -44,7 +44,7 @@ def test_exports_every_declared_symbol(lib):
             "ws_workspace_bytes", "ws_abi_version", "ws_status_string", "ws_last_error"} <= set(names)
     for name in names:
         assert hasattr(lib, name), name
-    assert lib.ws_abi_version() == 1
+    assert lib.ws_abi_version() == 2
     assert lib.ws_status_string(0) == b"WS_OK"
     assert lib.ws_status_string(10) == b"WS_ERR_HIP"
 
@@ -114,7 +114,7 @@ def test_step_errors(lib):
     h5 = Host(lens=(10, -1))
     assert step_call(lib, h5) == 2
     hw = Host(lens=(10, 200))            # 216 keys: the plan splits the KV range
-    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 2, 4, 16, 216) > 0
+    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 2, 4, 2, 16, 216) > 0
     assert step_call(lib, hw, wsp=None) == 9
     assert step_call(lib, hw, wsb=16) == 9
     assert step_call(lib, hw, wsp=FAKE + 4) == 9                       # misaligned workspace
@@ -193,9 +193,15 @@ def test_empty_calls_are_ok(lib):
 
 def test_workspace_bytes(lib):
     # a single 256-row tile per head needs KV splits (and partials) to fill the chip
-    n = lib.ws_workspace_bytes(ws.WS_OP_STEP, 1, 24, 256, 4352)
+    n = lib.ws_workspace_bytes(ws.WS_OP_STEP, 1, 24, 24, 256, 4352)
     assert n > 0 and n % (24 * 256 * 130 * 4) == 0
     # enough work items already: no splits, no workspace
-    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 4, 64, 512, 131584) == 0
-    assert lib.ws_workspace_bytes(ws.WS_OP_PREFILL, 2, 32, 16384, 16384) == 0
-    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 0, 24, 256, 4352) == 0
+    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 4, 64, 8, 512, 131584) == 0
+    # a 16-token block of 8 query heads per KV head packs into one 128-row
+    # tile per (stream, KV head): 32 tiles, so the long cache is split
+    n16 = lib.ws_workspace_bytes(ws.WS_OP_STEP, 4, 64, 8, 16, 131088)
+    assert n16 > 0 and n16 % (4 * 8 * 128 * 130 * 4) == 0
+    assert lib.ws_workspace_bytes(ws.WS_OP_PREFILL, 2, 32, 8, 16384, 16384) == 0
+    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 0, 24, 24, 256, 4352) == 0
+    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 1, 24, 5, 256, 4352) == 0   # 24 % 5 != 0
+    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 1, 24, 0, 256, 4352) == 0

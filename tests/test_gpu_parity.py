@@ -74,6 +74,16 @@ def test_step_ragged(D, Lq, lens):
     _check_full(wl, cache=cache)
 
 
+@pytest.mark.parametrize("out_dtype", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("Lq", [1, 16, 37])
+def test_step_small_block_gqa8(Lq, out_dtype):
+    """Small blocks of a GQA-8 model: the 8 query heads of a KV head share one
+    packed query tile (8 x Lq rows), and the long caches are split."""
+    wl = inputs.step_workload(f"step_gqa8_q{Lq}", 2, 16, 2, 128, Lq, [4100, 2500], seed=23 + Lq)
+    cache = gs.device_cache(wl, wl.cache_lens)
+    _check_full(wl, cache=cache, out_dtype=out_dtype)
+
+
 def test_step_mha_f32_out():
     wl = inputs.step_workload("step_mha_f32", 1, 6, 6, 128, 256, [1000], seed=13)
     cache = gs.device_cache(wl, wl.cache_lens)
