@@ -157,3 +157,23 @@ def test_rejected_call_changes_nothing():
     torch.cuda.synchronize()
     assert (out == 7.0).all() and (lse == 3.0).all()
     assert torch.equal(cache.k_pool.view(torch.int16), pool_before.view(torch.int16))
+
+
+
+def test_workspace_reuse():
+    """One workspace serves consecutive split-KV steps: every call gives the
+    same bits as a call with a freshly allocated workspace."""
+    wl = inputs.step_workload("ws_reuse", 2, 8, 2, 128, 40, [3000, 1800], seed=29)
+    cache = gs.device_cache(wl, wl.cache_lens)
+    gs.say("[gpu] workspace reuse over 4 steps")
+    host = torch.as_tensor(wl.cache_lens, dtype=torch.int32)
+    lens = (host, host.to(gs.dev()))
+    need = ws.workspace_bytes(ws.WS_OP_STEP, wl.B, wl.Hq, wl.Hkv, wl.Lq, int(host.max()) + wl.Lq)
+    assert need > 0
+    work = torch.full((need,), 0x5A, dtype=torch.uint8, device=gs.dev())   # contents are ignored
+    q, kn, vn = gs.to_dev_bf16(wl.q), gs.to_dev_bf16(wl.k_new), gs.to_dev_bf16(wl.v_new)
+    ref, ref_lse = ws.block_causal_attn_fwd(q, kn, vn, cache, lens, want_lse=True)
+    for _ in range(4):
+        out, lse = ws.block_causal_attn_fwd(q, kn, vn, cache, lens, want_lse=True, workspace=work)
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref) and torch.equal(lse, ref_lse)
