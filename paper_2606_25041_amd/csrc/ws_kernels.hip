@@ -596,6 +596,9 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     // land.
     static_assert(NW == 8, "two waves per SIMD");
     const bool lead = wave < NWD;
+    // a wave whose 32 rows all lie past the last row (a small block's tile)
+    // only takes part in the loads and barriers
+    const bool busy = q0 + wave * 32 < (int)nrows;
     Tile S;
     bf16x8 pf[NB][4];
     const int n_tiles = t_end - t_begin;
@@ -642,13 +645,15 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
             // hoist them out of the loop and hold them in registers the
             // pipeline needs.
             asm volatile("" : "+v"(kbase), "+v"(vbase[0]), "+v"(vbase[1]), "+v"(lofs_p), "+v"(lofs_k), "+v"(lofs_v));
-            if (j > t_begin) pv(stage_off(j - 1), pf);
-            if (j < t_end) qk(stage_off(j), S);
+            if (busy) {
+                if (j > t_begin) pv(stage_off(j - 1), pf);
+                if (j < t_end) qk(stage_off(j), S);
+            }
             wg_barrier();
             // the leading waves issue the loads of tile j+2 here, ahead of
             // their softmax, rather than ahead of their MFMA block
             if (lead && j + 2 < t_end) issue_tile(j + 2, (j + 2 - t_begin) % NSTAGE, pg_next);
-            if (j < t_end) softmax(j, S, pf);
+            if (busy && j < t_end) softmax(j, S, pf);
             // (read here, under the wait below: a scalar or LDS read left in
             // flight across the MFMA block would force full LDS drains there)
             if (lead && j + 3 < t_end) pg_next = page_of(j + 3);
