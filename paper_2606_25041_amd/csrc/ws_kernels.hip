@@ -702,7 +702,9 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
         } else if (!a.out_f32) {
             // bf16 output: o / l rounded to bf16 and the split's log2-domain
             // lse; register order, two accumulator groups (16 bytes) per
-            // lane, so each store instruction writes 1 KB contiguous
+            // lane, so each store instruction writes 1 KB contiguous.
+            // Partials are stored non-temporally (read once, by the combine
+            // launch)
             const int64_t blk = (((int64_t)split * a.B + b) * a.Hkv + kvh) * a.nrb + (r >> 5);
             const float inv = lt > 0.f ? 1.f / lt : 0.f;
             uint16_t *op = (uint16_t *)a.part_o + blk * (32 * D) + 8 * lane;
@@ -715,9 +717,9 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
                     val[2 * h + 0] = pack_bf16x2(o[n][md][4 * (g0 + h) + 0] * inv, o[n][md][4 * (g0 + h) + 1] * inv);
                     val[2 * h + 1] = pack_bf16x2(o[n][md][4 * (g0 + h) + 2] * inv, o[n][md][4 * (g0 + h) + 3] * inv);
                 }
-                *(u32x4 *)(op + pg * 512) = val;
+                __builtin_nontemporal_store(val, (u32x4 *)(op + pg * 512));
             }
-            if (hf == 0) a.part_ml[blk * 32 + l32] = lt > 0.f ? m[n] + __builtin_amdgcn_logf(lt) : -INFINITY;
+            if (hf == 0) __builtin_nontemporal_store(lt > 0.f ? m[n] + __builtin_amdgcn_logf(lt) : -INFINITY, a.part_ml + blk * 32 + l32);
         } else {
             // register order: each store instruction writes 1 KB contiguous
             const int64_t blk = (((int64_t)split * a.B + b) * a.Hkv + kvh) * a.nrb + (r >> 5);
@@ -729,11 +731,11 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
                     f32x4 val;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) val[e] = o[n][md][4 * g + e];
-                    *(f32x4 *)(op + (md * 4 + g) * 256) = val;
+                    __builtin_nontemporal_store(val, (f32x4 *)(op + (md * 4 + g) * 256));
                 }
             if (hf == 0) {
-                a.part_ml[2 * (blk * 32 + l32) + 0] = m[n];
-                a.part_ml[2 * (blk * 32 + l32) + 1] = lt;
+                __builtin_nontemporal_store(m[n], a.part_ml + 2 * (blk * 32 + l32) + 0);
+                __builtin_nontemporal_store(lt, a.part_ml + 2 * (blk * 32 + l32) + 1);
             }
         }
     }
