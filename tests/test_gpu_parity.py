@@ -7,6 +7,7 @@ import numpy as np
 import pytest
 import torch
 
+import paper_2606_25041_amd as ws
 from paper_2606_25041_amd import inputs
 from tests import gpu_support as gs
 
@@ -82,6 +83,33 @@ def test_step_small_block_gqa8(Lq, out_dtype):
     wl = inputs.step_workload(f"step_gqa8_q{Lq}", 2, 16, 2, 128, Lq, [4100, 2500], seed=23 + Lq)
     cache = gs.device_cache(wl, wl.cache_lens)
     _check_full(wl, cache=cache, out_dtype=out_dtype)
+
+
+def test_step_many_streams_lengths_from_memory():
+    """More streams than the cache lengths passed by value (32): the kernel
+    reads them from the device array; ragged lengths, GQA 2, d = 64."""
+    g = np.random.default_rng(31)
+    lens = [int(x) for x in g.integers(0, 700, size=40)]
+    wl = inputs.step_workload("step_b40", 40, 2, 1, 64, 8, lens, seed=31)
+    cache = gs.device_cache(wl, wl.cache_lens)
+    _check_full(wl, cache=cache)
+
+
+@pytest.mark.parametrize("out_dtype", [torch.bfloat16, torch.float32])
+def test_step_most_splits(out_dtype):
+    """One head, a 16-token block and an 8192-token cache: the plan uses the
+    largest split count (32), so the merge sees every split slot."""
+    wl = inputs.step_workload("step_s32", 1, 1, 1, 128, 16, [8192], seed=37)
+    cache = gs.device_cache(wl, wl.cache_lens)
+    assert ws.workspace_bytes(ws.WS_OP_STEP, 1, 1, 1, 16, 8192 + 16) == 32 * 1 * 32 * 130 * 4
+    _check_full(wl, cache=cache, out_dtype=out_dtype)
+
+
+def test_step_one_token_empty_cache():
+    """The smallest step: one new token, nothing cached (it sees itself)."""
+    wl = inputs.step_workload("step_min", 2, 4, 2, 128, 1, [0, 0], seed=41)
+    cache = gs.device_cache(wl, wl.cache_lens)
+    _check_full(wl, cache=cache)
 
 
 def test_step_mha_f32_out():
