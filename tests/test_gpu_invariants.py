@@ -177,3 +177,38 @@ def test_workspace_reuse():
         out, lse = ws.block_causal_attn_fwd(q, kn, vn, cache, lens, want_lse=True, workspace=work)
         torch.cuda.synchronize()
         assert torch.equal(out, ref) and torch.equal(lse, ref_lse)
+
+
+def test_solver_loop_then_commit():
+    """The performer's loop (Sec. 2.4, Sec. 2.1): several solver steps of a
+    noisy block attend to a fixed cache without changing it, then the clean
+    block is committed.  Every step matches the oracle, the pool is bitwise
+    unchanged until the commit, and the commit equals the oracle's append."""
+    B, Hq, Hkv, D, Lq = 2, 8, 2, 128, 48
+    lens = [700, 333]
+    base = inputs.step_workload("solver_cache", B, Hq, Hkv, D, Lq, lens, seed=43)
+    cache = gs.device_cache(base, base.cache_lens)
+    pool_k0 = cache.k_pool.clone()
+    pool_v0 = cache.v_pool.clone()
+    gs.say("[gpu] solver loop: 3 uncommitted steps, then a committing step")
+    wl = inputs.step_workload("solver_step", B, Hq, Hkv, D, Lq, lens, seed=43)
+    for s in range(4):
+        # the noisy block changes every step (its queries, keys and values);
+        # the cached keys and values stay the same
+        wl.q = inputs.bf16_normal(inputs.rng(500 + s, inputs.S_Q), tuple(wl.q.shape))
+        wl.k[:, wl.Lc_max:] = inputs.bf16_normal(inputs.rng(500 + s, inputs.S_K), tuple(wl.k_new.shape))
+        wl.v[:, wl.Lc_max:] = inputs.bf16_normal(inputs.rng(500 + s, inputs.S_V), tuple(wl.v_new.shape))
+        commit = s == 3
+        out, lse = gs.run_gpu(wl, cache=cache, fuse=commit)
+        torch.cuda.synchronize()
+        ref, ref_lse = gs.run_oracle(wl)
+        gs.assert_close(gs.compare(out, lse, ref, ref_lse))
+        if not commit:
+            assert torch.equal(cache.k_pool.view(torch.int16), pool_k0.view(torch.int16))
+            assert torch.equal(cache.v_pool.view(torch.int16), pool_v0.view(torch.int16))
+    # the committed pool: the oracle appends the last step's block after each stream's cache
+    pk = pool_k0.view(torch.int16).cpu().numpy().view(np.uint16).copy()
+    pv = pool_v0.view(torch.int16).cpu().numpy().view(np.uint16).copy()
+    oracle.kv_append(pk, pv, wl.page_table, np.asarray(lens), inputs.bf16_bits(wl.k_new), inputs.bf16_bits(wl.v_new))
+    assert np.array_equal(cache.k_pool.view(torch.int16).cpu().numpy().view(np.uint16), pk)
+    assert np.array_equal(cache.v_pool.view(torch.int16).cpu().numpy().view(np.uint16), pv)
