@@ -213,6 +213,10 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int hf = lane >> 5;     // which half of the wave
     const int l32 = lane & 31;
+    // 32-row block of the tile this wave computes: the trailing waves (which
+    // issue no tile loads) take the first blocks, so a small block's rows go
+    // to waves without load duty
+    const int rblk = (wave + NW / 2) % NW;
 
     // Query rows of this wave go global -> LDS -> registers, issued first
     // thing: the direct loads stay in order with the tile loads, so one
@@ -230,7 +234,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
         for (int i = 0; i < QI; ++i) {
             const int r = i * RPW + lane / LPR;   // row within the wave's 32
             const int ch = (lane % LPR) ^ swz<D>(r);
-            const int p = min(q0 + wave * 32 + r, (int)nrows - 1);
+            const int p = min(q0 + rblk * 32 + r, (int)nrows - 1);
             const int t = row_token(p);
             const int h = row_head(p, t);
             dma16(qg + (int64_t)t * (2 * q_st) + (int64_t)h * (2 * q_sh) + 16 * ch, lds_addr(smem) + q_stage + i * 1024);
@@ -269,13 +273,13 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     };
 
     // ---- this lane's query rows -------------------------------------------
-    // row n of the lane: q0 + wave * 32 * NB + 32 * n + l32 (the fragments
+    // row n of the lane: q0 + rblk * 32 * NB + 32 * n + l32 (the fragments
     // are staged through LDS in the pipeline prologue, below)
     int row[NB], kend[NB], tok[NB], hqr[NB];
     bf16x8 qf[NB][KK];
 #pragma unroll
     for (int n = 0; n < NB; ++n) {
-        row[n] = q0 + wave * 32 * NB + 32 * n + l32;
+        row[n] = q0 + rblk * 32 * NB + 32 * n + l32;
         const int pc = min(row[n], (int)nrows - 1);
         tok[n] = row_token(pc);
         hqr[n] = row_head(pc, tok[n]);
@@ -598,7 +602,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     const bool lead = wave < NWD;
     // a wave whose 32 rows all lie past the last row (a small block's tile)
     // only takes part in the loads and barriers
-    const bool busy = q0 + wave * 32 < (int)nrows;
+    const bool busy = q0 + rblk * 32 < (int)nrows;
     Tile S;
     bf16x8 pf[NB][4];
     const int n_tiles = t_end - t_begin;
