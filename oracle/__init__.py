@@ -6,7 +6,9 @@ Python binding never import it.
 
 * ``prefill`` / ``step`` wrap the plain C triple loop in ``ws_oracle.c``
   (block-causal attention, Wan-Streamer v0.1 Abstract, Sec. 1 and Fig. 1;
-  conditioning set of Sec. 2.1, Eq. 1).
+  conditioning set of Sec. 2.1, Eq. 1), optionally with a token-causal
+  segment at the end of each block (the thinker's language and state slots,
+  Sec. 1 and Sec. 2.4).
 * ``kv_append`` / ``gather`` are the paged full-history cache written out as
   plain per-token loops (the performer appends each received KV slice to its
   own full-history cache, Sec. 2.4).
@@ -46,6 +48,10 @@ def _bind(lib):
     lib.wso_prefill.restype = I
     lib.wso_step.argtypes = [P, P, P, P, P, I, I, I, I, P, I, I, I, D, P, I64, P, P, P, I]
     lib.wso_step.restype = I
+    lib.wso_prefill_text.argtypes = [P, P, P, I, I, I, I, I, I, P, I, P, D, P, I64, P, P, P, I]
+    lib.wso_prefill_text.restype = I
+    lib.wso_step_text.argtypes = [P, P, P, P, P, I, I, I, I, P, P, I, I, I, D, P, I64, P, P, P, I]
+    lib.wso_step_text.restype = I
     lib.wso_mutant.restype = I
     return lib
 
@@ -70,11 +76,14 @@ def _ptr(a):
     return a.ctypes.data_as(ctypes.c_void_p) if a is not None else None
 
 
-def prefill(q, k, v, offsets, scale, rows=None, want_probs=False, nthreads=None, lib=None):
+def prefill(q, k, v, offsets, scale, rows=None, want_probs=False, nthreads=None, lib=None,
+            text_starts=None):
     """Block-causal attention over whole sequences.
 
     q: [B][L][Hq][d]; k, v: [B][L][Hkv][d]; offsets: [B][nb+1] int block
-    boundaries (first 0, non-decreasing, last L).  rows: optional int array
+    boundaries (first 0, non-decreasing, last L).  text_starts: optional
+    [B][nb] start of each block's token-causal segment (its block end: no
+    segment; Sec. 1, Sec. 2.4).  rows: optional int array
     [n][3] of (b, h, i).  Returns (out, lse[, probs]): with rows=None,
     out [B][L][Hq][d] and lse [B][Hq][L]; with rows, out [n][d], lse [n] and
     probs [n][L].
@@ -99,19 +108,24 @@ def prefill(q, k, v, offsets, scale, rows=None, want_probs=False, nthreads=None,
         out = np.empty((n, d), np.float64)
         lse = np.empty((n,), np.float64)
         probs = np.zeros((n, L), np.float64) if want_probs else None
-    rc = lib.wso_prefill(_ptr(q), _ptr(k), _ptr(v), dt, B, L, Hq, Hkv, d,
-                         _ptr(offsets), nb, float(scale), _ptr(rows_a), n,
-                         _ptr(out), _ptr(lse), _ptr(probs),
-                         int(nthreads or default_threads()))
+    ts = None
+    if text_starts is not None:
+        ts = np.ascontiguousarray(np.asarray(text_starts, dtype=np.int32).reshape(B, nb))
+    rc = lib.wso_prefill_text(_ptr(q), _ptr(k), _ptr(v), dt, B, L, Hq, Hkv, d,
+                              _ptr(offsets), nb, _ptr(ts), float(scale), _ptr(rows_a), n,
+                              _ptr(out), _ptr(lse), _ptr(probs),
+                              int(nthreads or default_threads()))
     if rc != 0:
         raise ValueError(f"oracle prefill rejected its arguments (rc={rc})")
     return (out, lse, probs) if want_probs else (out, lse)
 
 
 def step(q, k_cache, v_cache, cache_lens, k_new, v_new, scale, rows=None,
-         want_probs=False, nthreads=None, lib=None):
+         want_probs=False, nthreads=None, lib=None, text_starts=None):
     """One streaming step: the new block attends to its stream's cache
-    (tokens [0, cache_lens[b])) and bidirectionally to itself.
+    (tokens [0, cache_lens[b])) and bidirectionally to itself, except for an
+    optional token-causal segment starting at text_starts[b] within the
+    block (Lq: none).
 
     q: [B][Lq][Hq][d]; k_cache, v_cache: [B][Lc_max][Hkv][d] logical cache;
     k_new, v_new: [B][Lq][Hkv][d].  Returns like ``prefill``; probs rows have
@@ -140,10 +154,13 @@ def step(q, k_cache, v_cache, cache_lens, k_new, v_new, scale, rows=None,
         out = np.empty((n, d), np.float64)
         lse = np.empty((n,), np.float64)
         probs = np.zeros((n, Lc_max + Lq), np.float64) if want_probs else None
-    rc = lib.wso_step(_ptr(q), _ptr(kc), _ptr(vc), _ptr(kn), _ptr(vn), dt,
-                      B, Lq, Lc_max, _ptr(lens), Hq, Hkv, d, float(scale),
-                      _ptr(rows_a), n, _ptr(out), _ptr(lse), _ptr(probs),
-                      int(nthreads or default_threads()))
+    ts = None
+    if text_starts is not None:
+        ts = np.ascontiguousarray(np.asarray(text_starts, dtype=np.int32).reshape(B))
+    rc = lib.wso_step_text(_ptr(q), _ptr(kc), _ptr(vc), _ptr(kn), _ptr(vn), dt,
+                           B, Lq, Lc_max, _ptr(lens), _ptr(ts), Hq, Hkv, d, float(scale),
+                           _ptr(rows_a), n, _ptr(out), _ptr(lse), _ptr(probs),
+                           int(nthreads or default_threads()))
     if rc != 0:
         raise ValueError(f"oracle step rejected its arguments (rc={rc})")
     return (out, lse, probs) if want_probs else (out, lse)

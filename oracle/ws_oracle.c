@@ -15,6 +15,15 @@
  *   id beta_k(j) is <= beta_q, i.e. its own block in both directions and
  *   every earlier block;
  *
+ *   optionally, each block ends in a token-causal segment (the thinker's
+ *   language and state slots, decoded token by token: Sec. 1, Sec. 2.4;
+ *   language tokens are trained by next-token prediction, Sec. 2.1) that
+ *   starts at position tau of the block.  Inside such a block the tokens
+ *   before tau still see each other in both directions but not the
+ *   segment, and a segment token at position i sees the tokens before tau
+ *   and the segment tokens at positions <= i.  Earlier blocks stay fully
+ *   visible;
+ *
  *   o_i   = sum_{j visible} softmax_j(scale * <q_i, k_j>) v_j
  *   lse_i = m_i + ln(sum_{j visible} exp(scale * <q_i, k_j> - m_i)),
  *           m_i = max_{j visible} scale * <q_i, k_j>.
@@ -78,6 +87,10 @@ typedef struct {
     /* step: keys are cache tokens [0, Lc[b]) followed by the Lq new tokens */
     wso_view kc, vc;
     const int32_t *cache_lens;
+    /* start of each block's token-causal segment, or NULL for none.
+     * prefill: [B][nb] absolute positions; step: [B] positions within the
+     * new block */
+    const int32_t *text_starts;
     /* row list: nrows triples (b, h, i); NULL means every row */
     const int32_t *rows;
     int64_t nrows;
@@ -143,12 +156,23 @@ static void wso_row(const wso_job *J, wso_scratch *S, int b, int h, int64_t i,
     const int64_t Lk = wso_num_keys(J, b);
     const int d = J->d;
 
-    /* 1. explicit mask row from block ids */
+    /* 1. explicit mask row from block ids (and the token-causal segment of
+     * the query's block).  Positions are in key order: the query sits at
+     * key position iq, its block's segment starts at key position tau (-1:
+     * the block has none). */
     int beta_q;
-    if (J->kind == WSO_PREFILL)
+    int64_t iq, tau = -1;
+    if (J->kind == WSO_PREFILL) {
         beta_q = wso_block_of(J->offsets + (int64_t)b * (J->nb + 1), J->nb, i);
-    else
+        iq = i;
+        if (J->text_starts)
+            tau = J->text_starts[(int64_t)b * J->nb + beta_q];
+    } else {
         beta_q = 1;
+        iq = (int64_t)J->cache_lens[b] + i;
+        if (J->text_starts)
+            tau = (int64_t)J->cache_lens[b] + J->text_starts[b];
+    }
     for (int64_t j = 0; j < Lk; ++j) {
         int beta_k;
         if (J->kind == WSO_PREFILL)
@@ -156,12 +180,24 @@ static void wso_row(const wso_job *J, wso_scratch *S, int b, int h, int64_t i,
         else
             beta_k = (j < J->cache_lens[b]) ? 0 : 1;
 #if WSO_MUTANT == 1
-        S->mask[j] = (unsigned char)(beta_k < beta_q);
+        int vis = beta_k < beta_q;
 #elif WSO_MUTANT == 8
-        S->mask[j] = (unsigned char)(beta_k >= beta_q);
+        int vis = beta_k >= beta_q;
 #else
-        S->mask[j] = (unsigned char)(beta_k <= beta_q);
+        int vis = beta_k <= beta_q;
 #endif
+        if (vis && beta_k == beta_q && tau >= 0) {
+            /* same block: a key of the segment is visible only to segment
+             * queries at or after it */
+#if WSO_MUTANT == 9
+            vis = j < tau || j <= iq + 1;
+#elif WSO_MUTANT == 10
+            vis = j < tau || j <= iq || iq < tau;
+#else
+            vis = j < tau || j <= iq;
+#endif
+        }
+        S->mask[j] = (unsigned char)vis;
     }
 
     /* 2. logits of visible keys, and their maximum */
@@ -343,15 +379,18 @@ static int wso_check_common(int B, int Lq, int Hq, int Hkv, int d)
  * Whole-sequence block-causal attention.  q, k, v: [B][L][H][d] contiguous
  * (dtype WSO_F64 or WSO_BF16 bit patterns).  offsets: [B][nb+1] block
  * boundaries, offsets[b][0] = 0, non-decreasing, offsets[b][nb] = L.
+ * text_starts: NULL, or [B][nb] start of each block's token-causal segment
+ * (offsets[b][n] <= text_starts[b][n] <= offsets[b][n+1]; equal to the
+ * block end: no segment).
  * rows: NULL for every row, else nrows triples (b, h, i).  probs (row list
  * only, may be NULL): [nrows][L] normalised attention weights.
  * Returns 0 on success, -2 on bad arguments, -1 on allocation failure.
  */
-int wso_prefill(const void *q, const void *k, const void *v, int dtype,
-                int B, int L, int Hq, int Hkv, int d,
-                const int32_t *offsets, int nb, double scale,
-                const int32_t *rows, int64_t nrows,
-                double *out, double *lse, double *probs, int nthreads)
+int wso_prefill_text(const void *q, const void *k, const void *v, int dtype,
+                     int B, int L, int Hq, int Hkv, int d,
+                     const int32_t *offsets, int nb, const int32_t *text_starts, double scale,
+                     const int32_t *rows, int64_t nrows,
+                     double *out, double *lse, double *probs, int nthreads)
 {
     if (wso_check_common(B, L, Hq, Hkv, d) || nb < 0 || !offsets || !out)
         return -2;
@@ -359,9 +398,15 @@ int wso_prefill(const void *q, const void *k, const void *v, int dtype,
         const int32_t *off = offsets + (int64_t)b * (nb + 1);
         if (off[0] != 0 || off[nb] != L)
             return -2;
-        for (int n = 0; n < nb; ++n)
+        for (int n = 0; n < nb; ++n) {
             if (off[n + 1] < off[n])
                 return -2;
+            if (text_starts) {
+                const int32_t t = text_starts[(int64_t)b * nb + n];
+                if (t < off[n] || t > off[n + 1])
+                    return -2;
+            }
+        }
     }
     wso_job J;
     memset(&J, 0, sizeof J);
@@ -373,6 +418,7 @@ int wso_prefill(const void *q, const void *k, const void *v, int dtype,
     J.v = (wso_view){v, dtype, (int64_t)L * Hkv * d, (int64_t)Hkv * d, d};
     J.offsets = offsets;
     J.nb = nb;
+    J.text_starts = text_starts;
     J.rows = rows;
     J.nrows = nrows;
     J.out = out;
@@ -382,25 +428,42 @@ int wso_prefill(const void *q, const void *k, const void *v, int dtype,
     return wso_run(&J, nthreads);
 }
 
+/* The same with no token-causal segments (pure block-causal attention). */
+int wso_prefill(const void *q, const void *k, const void *v, int dtype,
+                int B, int L, int Hq, int Hkv, int d,
+                const int32_t *offsets, int nb, double scale,
+                const int32_t *rows, int64_t nrows,
+                double *out, double *lse, double *probs, int nthreads)
+{
+    return wso_prefill_text(q, k, v, dtype, B, L, Hq, Hkv, d, offsets, nb, NULL, scale,
+                            rows, nrows, out, lse, probs, nthreads);
+}
+
 /*
  * One streaming step: the Lq tokens of a new block attend to the cache
  * tokens [0, cache_lens[b]) of their stream (all earlier blocks) and to the
  * whole new block (their own block).  kc, vc: [B][Lc_max][Hkv][d]; q: [B][Lq][Hq][d];
  * kn, vn: [B][Lq][Hkv][d]; all contiguous.  probs rows have length
  * Lc_max + Lq (entries past the stream's own key count are left untouched).
+ * text_starts: NULL, or [B] start of the new block's token-causal segment
+ * within the block (0 <= text_starts[b] <= Lq; Lq: no segment).
  */
-int wso_step(const void *q, const void *kc, const void *vc,
-             const void *kn, const void *vn, int dtype,
-             int B, int Lq, int Lc_max, const int32_t *cache_lens,
-             int Hq, int Hkv, int d, double scale,
-             const int32_t *rows, int64_t nrows,
-             double *out, double *lse, double *probs, int nthreads)
+int wso_step_text(const void *q, const void *kc, const void *vc,
+                  const void *kn, const void *vn, int dtype,
+                  int B, int Lq, int Lc_max, const int32_t *cache_lens,
+                  const int32_t *text_starts,
+                  int Hq, int Hkv, int d, double scale,
+                  const int32_t *rows, int64_t nrows,
+                  double *out, double *lse, double *probs, int nthreads)
 {
     if (wso_check_common(B, Lq, Hq, Hkv, d) || Lc_max < 0 || !cache_lens || !out)
         return -2;
-    for (int b = 0; b < B; ++b)
+    for (int b = 0; b < B; ++b) {
         if (cache_lens[b] < 0 || cache_lens[b] > Lc_max)
             return -2;
+        if (text_starts && (text_starts[b] < 0 || text_starts[b] > Lq))
+            return -2;
+    }
     wso_job J;
     memset(&J, 0, sizeof J);
     J.kind = WSO_STEP;
@@ -412,6 +475,7 @@ int wso_step(const void *q, const void *kc, const void *vc,
     J.kc = (wso_view){kc, dtype, (int64_t)Lc_max * Hkv * d, (int64_t)Hkv * d, d};
     J.vc = (wso_view){vc, dtype, (int64_t)Lc_max * Hkv * d, (int64_t)Hkv * d, d};
     J.cache_lens = cache_lens;
+    J.text_starts = text_starts;
     J.rows = rows;
     J.nrows = nrows;
     J.out = out;
@@ -419,6 +483,18 @@ int wso_step(const void *q, const void *kc, const void *vc,
     J.probs = rows ? probs : NULL;
     J.lk_max = (int64_t)Lc_max + Lq;
     return wso_run(&J, nthreads);
+}
+
+/* The same with no token-causal segment in the new block. */
+int wso_step(const void *q, const void *kc, const void *vc,
+             const void *kn, const void *vn, int dtype,
+             int B, int Lq, int Lc_max, const int32_t *cache_lens,
+             int Hq, int Hkv, int d, double scale,
+             const int32_t *rows, int64_t nrows,
+             double *out, double *lse, double *probs, int nthreads)
+{
+    return wso_step_text(q, kc, vc, kn, vn, dtype, B, Lq, Lc_max, cache_lens, NULL, Hq, Hkv, d,
+                         scale, rows, nrows, out, lse, probs, nthreads);
 }
 
 int wso_mutant(void) { return WSO_MUTANT; }

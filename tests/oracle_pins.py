@@ -11,7 +11,12 @@ The rule being pinned (Wan-Streamer v0.1, Abstract, Sec. 1 with Fig. 1 and
 Sec. 5: block-causal attention over the interleaved stream; Sec. 2.1, Eq. 1:
 unit k is conditioned on inputs of units <= k and responses of units < k):
 a token sees every token of its own block and of every earlier block, and
-nothing later.
+nothing later.  With a token-causal segment at the end of a block (the
+thinker's language and state slots, decoded token by token: Sec. 1 and
+Sec. 2.4; next-token prediction of language, Sec. 2.1), the block's
+observation tokens (before the segment) see each other but not the segment,
+and a segment token sees the observations and the segment tokens up to
+itself.
 """
 import itertools
 import math
@@ -304,6 +309,120 @@ def pin_row_subset_matches_all_rows(lib):
         assert np.array_equal(o2[r], out[b, i, h]) and l2[r] == lse[b, h, i]
 
 
+# --------------------------------------------------------------------------
+# token-causal segments at the end of blocks
+
+def _brute_force_text_row(q, k, v, ids, starts, i, scale):
+    """Independent pure-Python rule for one query row: a token is an
+    observation of its block before the block's segment start and a segment
+    (text) token from there on; earlier blocks are always visible, and inside
+    the block observations are visible to everyone there while segment
+    tokens are visible only to segment tokens at or after them."""
+    role = ["text" if j >= starts[ids[j]] else "obs" for j in range(len(ids))]
+    visible = {j for j in range(len(ids))
+               if ids[j] < ids[i] or (ids[j] == ids[i] and (role[j] == "obs" or (role[i] == "text" and j <= i)))}
+    logits = {j: scale * math.fsum(q[i][c] * k[j][c] for c in range(len(q[i]))) for j in visible}
+    m = max(logits.values())
+    w = {j: math.exp(logits[j] - m) for j in visible}
+    z = math.fsum(w.values())
+    out = [math.fsum(w[j] * v[j][c] for j in sorted(visible)) / z for c in range(len(v[0]))]
+    return out, m + math.log(z)
+
+
+def pin_bruteforce_text_segments(lib, n=8, d=3):
+    """Every block composition of 8 tokens with every choice of segment
+    start in every block (11144 cases) against the pure-Python rule."""
+    rng = _rng(31)
+    q = rng.standard_normal((1, n, 1, d))
+    k = rng.standard_normal((1, n, 1, d))
+    v = rng.standard_normal((1, n, 1, d))
+    ql, kl, vl = q[0, :, 0].tolist(), k[0, :, 0].tolist(), v[0, :, 0].tolist()
+    scale = 0.8
+    cases = 0
+    for comp in range(2 ** (n - 1)):
+        cuts = [g + 1 for g in range(n - 1) if comp >> g & 1]
+        offs = [0] + cuts + [n]
+        ids = [sum(1 for c in cuts if c <= t) for t in range(n)]
+        choices = [range(offs[b], offs[b + 1] + 1) for b in range(len(offs) - 1)]
+        for starts in itertools.product(*choices):
+            out, lse = oracle.prefill(q, k, v, np.array([offs], np.int32), scale, nthreads=1, lib=lib,
+                                      text_starts=np.array([starts], np.int32))
+            for i in range(n):
+                ref_o, ref_lse = _brute_force_text_row(ql, kl, vl, ids, starts, i, scale)
+                assert np.max(np.abs(out[0, i, 0] - ref_o)) <= ATOL_TIGHT, (comp, starts, i)
+                assert abs(lse[0, 0, i] - ref_lse) <= ATOL_TIGHT, (comp, starts, i)
+            cases += 1
+    assert cases == 11144
+
+
+def pin_text_everywhere_is_causal_attention(lib):
+    """Blocks that are all segment (start = block start) make every token
+    see exactly the tokens up to itself: standard causal attention, whatever
+    the block boundaries (fp64 SDPA is_causal)."""
+    rng = _rng(32)
+    B, L, H, d = 2, 31, 2, 8
+    q, k, v = (rng.standard_normal((B, L, H, d)) for _ in range(3))
+    offs = np.stack([_random_offsets(rng, L, 6) for _ in range(B)])
+    out, lse = oracle.prefill(q, k, v, offs, 0.45, lib=lib, text_starts=offs[:, :-1])
+    assert np.max(np.abs(out - _sdpa(q, k, v, 0.45, causal=True))) <= 1e-12
+    assert np.max(np.abs(lse - _lse_ref(q, k, 0.45, True))) <= 1e-12
+
+
+def pin_empty_segments_are_block_causal(lib):
+    """Segments that start at the block end are empty: bitwise the plain
+    block-causal result."""
+    rng = _rng(33)
+    B, L, H, Hkv, d = 2, 27, 4, 2, 5
+    q = rng.standard_normal((B, L, H, d))
+    k = rng.standard_normal((B, L, Hkv, d))
+    v = rng.standard_normal((B, L, Hkv, d))
+    offs = np.stack([_random_offsets(rng, L, 5) for _ in range(B)])
+    o1, l1 = oracle.prefill(q, k, v, offs, 0.6, lib=lib)
+    o2, l2 = oracle.prefill(q, k, v, offs, 0.6, lib=lib, text_starts=offs[:, 1:])
+    assert np.array_equal(o1, o2) and np.array_equal(l1, l2)
+
+
+def pin_zero_query_text_counts(lib):
+    """Q = 0: o_i is the mean of the visible values and lse_i = ln(#visible).
+    An observation token of block b sees [0, start_b); a segment token at i
+    sees [0, i]."""
+    rng = _rng(34)
+    B, L, H, d = 1, 40, 1, 4
+    q = np.zeros((B, L, H, d))
+    k = rng.standard_normal((B, L, H, d))
+    v = rng.standard_normal((B, L, H, d))
+    offs = np.array([[0, 3, 4, 11, 11, 25, 40]], np.int32)
+    starts = np.array([[1, 4, 8, 11, 25, 33]], np.int32)   # empty, whole, inner, empty block, empty, inner
+    out, lse = oracle.prefill(q, k, v, offs, 0.9, lib=lib, text_starts=starts)
+    for i in range(L):
+        blk = next(b for b in range(6) if offs[0, b] <= i < offs[0, b + 1])
+        n = int(starts[0, blk]) if i < starts[0, blk] else i + 1
+        assert np.max(np.abs(out[0, i, 0] - v[0, :n, 0].mean(axis=0))) <= 1e-13, i
+        assert abs(lse[0, 0, i] - math.log(n)) <= 1e-13, i
+
+
+def pin_streaming_equals_prefill_text(lib):
+    """Prefill rows of block j equal a streaming step of block j (its segment
+    start given relative to the block) over a cache of blocks < j."""
+    rng = _rng(35)
+    B, H, Hkv, d = 2, 4, 2, 6
+    lengths = [6, 4, 9, 5]
+    rel = [[2, 4, 0, 5], [6, 1, 9, 3]]    # per stream, segment start within each block
+    L = sum(lengths)
+    q = rng.standard_normal((B, L, H, d))
+    k = rng.standard_normal((B, L, Hkv, d))
+    v = rng.standard_normal((B, L, Hkv, d))
+    offs = _offsets_from_lengths(lengths)
+    starts = np.array([[offs[j] + r[j] for j in range(4)] for r in rel], np.int32)
+    out, lse = oracle.prefill(q, k, v, np.stack([offs] * B), 0.7, lib=lib, text_starts=starts)
+    for j in range(len(lengths)):
+        s, e = int(offs[j]), int(offs[j + 1])
+        so, sl = oracle.step(q[:, s:e], k[:, :s], v[:, :s], [s] * B, k[:, s:e], v[:, s:e], 0.7,
+                             lib=lib, text_starts=[r[j] for r in rel])
+        assert np.array_equal(so, out[:, s:e]), j
+        assert np.array_equal(sl, lse[:, :, s:e]), j
+
+
 ALL_PINS = [
     pin_bruteforce_all_compositions,
     pin_single_block_is_full_attention,
@@ -319,6 +438,11 @@ ALL_PINS = [
     pin_step_ragged_cache_lengths,
     pin_bf16_inputs_are_widened_exactly,
     pin_row_subset_matches_all_rows,
+    pin_bruteforce_text_segments,
+    pin_text_everywhere_is_causal_attention,
+    pin_empty_segments_are_block_causal,
+    pin_zero_query_text_counts,
+    pin_streaming_equals_prefill_text,
 ]
 
 # the deliberately broken oracle builds (see WSO_MUTANT in ws_oracle.c)
@@ -331,4 +455,6 @@ MUTANTS = {
     6: "block boundary off by one",
     7: "output not normalised",
     8: "mask direction reversed",
+    9: "segment token sees the next segment token",
+    10: "observation tokens see their block's segment",
 }
