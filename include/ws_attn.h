@@ -19,6 +19,17 @@
  *   lse_i = natural log of the softmax denominator (including its max shift)
  * Grouped-query attention: query head h reads KV head h / (Hq / Hkv).
  *
+ * Token-causal segments (the *_text entry points).  The thinker decodes the
+ * language and state slots of a unit token by token (Sec. 1, Sec. 2.4;
+ * language is trained by next-token prediction, Sec. 2.1).  A block may end
+ * in such a segment, starting at position tau of the block: the block's
+ * tokens before tau (its observations) see each other in both directions
+ * but not the segment, and a segment token at position i sees the
+ * observations and the segment tokens at positions <= i.  Earlier blocks
+ * stay fully visible.  So token i of a block sees exactly the keys
+ * j < max(tau, i + 1); tau = block end means no segment (plain
+ * block-causal), tau = block start makes the block token-causal.
+ *
  * Conventions for every entry point
  * ---------------------------------
  * - Token tensors are 4-d [batch][tokens][heads][head_dim] described by
@@ -57,7 +68,7 @@
 extern "C" {
 #endif
 
-#define WS_ABI_VERSION 2
+#define WS_ABI_VERSION 3
 #define WS_PAGE_SIZE 64
 
 typedef enum {
@@ -66,7 +77,8 @@ typedef enum {
     WS_ERR_SHAPE = 2,       /* a size is negative or sizes are inconsistent  */
     WS_ERR_UNSUPPORTED = 3, /* head_dim, dtype or page_size not supported    */
     WS_ERR_ALIGN = 4,       /* pointer not 16-byte aligned / stride % 8 != 0 */
-    WS_ERR_OFFSETS = 5,     /* block offsets: first != 0, decreasing, last != seq_len */
+    WS_ERR_OFFSETS = 5,     /* block offsets: first != 0, decreasing, last != seq_len;
+                               or a token-causal segment start outside its block */
     WS_ERR_PAGE = 6,        /* a page id that would be touched is outside [0, num_pages) */
     WS_ERR_CAPACITY = 7,    /* tokens exceed max_pages_per_seq * page_size   */
     WS_ERR_HEADS = 8,       /* num_q_heads % num_kv_heads != 0, or head counts differ from the cache's */
@@ -202,7 +214,50 @@ int ws_block_causal_prefill(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v,
                             float scale, ws_tensor4 out, float *lse, void *stream);
 
 /*
- * Workspace bytes ws_block_causal_attn_fwd needs for this shape (op =
+ * ws_block_causal_attn_fwd_text -- a streaming step whose new block ends in
+ * a token-causal segment (the thinker's pass over the language and state
+ * slots, Sec. 1 and Sec. 2.4).  Same arguments and errors as
+ * ws_block_causal_attn_fwd, plus
+ *   text_starts_host / _dev: int32 [batch], same values on host and device:
+ *                the segment of stream b's new block starts at token
+ *                text_starts[b] of the block, 0 <= text_starts[b] <= new_len
+ *                (new_len: no segment; 0: the block is token-causal).  New
+ *                token t sees cache tokens [0, cache_lens[b]) and new tokens
+ *                [0, max(text_starts[b], t + 1)).
+ * A start outside [0, new_len] gives WS_ERR_OFFSETS.  Workspace as for
+ * ws_block_causal_attn_fwd.
+ */
+int ws_block_causal_attn_fwd_text(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new,
+                                  const ws_paged_kv *kv,
+                                  const int32_t *cache_lens_host, const int32_t *cache_lens_dev,
+                                  const int32_t *text_starts_host, const int32_t *text_starts_dev,
+                                  int32_t batch, int32_t new_len, int32_t num_q_heads,
+                                  float scale, int32_t flags,
+                                  ws_tensor4 out, float *lse,
+                                  void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * ws_block_causal_prefill_text -- whole sequences whose blocks end in
+ * token-causal segments (the thinker's language and state slots, Sec. 1 and
+ * Sec. 2.4).  Same arguments and errors as ws_block_causal_prefill, plus
+ *   text_starts_host / _dev: int32 [batch][num_blocks], same values: the
+ *          segment of block n of stream b starts at absolute token
+ *          text_starts[b][n], block_offsets[b][n] <= text_starts[b][n] <=
+ *          block_offsets[b][n+1] (the block end: no segment).  Token i of
+ *          block n sees every token j < max(text_starts[b][n], i + 1).
+ * A start outside its block gives WS_ERR_OFFSETS.
+ */
+int ws_block_causal_prefill_text(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v,
+                                 const ws_paged_kv *kv_or_null,
+                                 const int32_t *block_offsets_host, const int32_t *block_offsets_dev,
+                                 const int32_t *text_starts_host, const int32_t *text_starts_dev,
+                                 int32_t batch, int32_t seq_len, int32_t num_blocks,
+                                 int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                 float scale, ws_tensor4 out, float *lse, void *stream);
+
+/*
+ * Workspace bytes ws_block_causal_attn_fwd (and its _text variant) needs
+ * for this shape (op =
  * WS_OP_STEP; num_kv_heads = the cache's; max_k = largest cache_lens[b] +
  * new_len).  WS_OP_PREFILL returns 0.  Pure host arithmetic; returns 0 for
  * invalid arguments.

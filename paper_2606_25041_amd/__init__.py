@@ -7,8 +7,10 @@ If the library is missing this module raises; there is no fallback.
 
 Entry points (same names as the C ABI, without the ``ws_`` prefix):
   kv_append(cache, cache_lens, k_new, v_new)
-  block_causal_attn_fwd(q, k_new, v_new, cache, cache_lens, ...)
-  block_causal_prefill(q, k, v, block_offsets, ...)
+  block_causal_attn_fwd(q, k_new, v_new, cache, cache_lens, ..., text_starts=None)
+  block_causal_prefill(q, k, v, block_offsets, ..., text_starts=None)
+(with text_starts: the *_text entry points, blocks ending in a token-causal
+segment)
   workspace_bytes(op, batch, num_q_heads, num_kv_heads, max_q, max_k)
 """
 import ctypes
@@ -80,7 +82,15 @@ def library():
         lib.ws_block_causal_prefill.argtypes = [
             Tensor4, Tensor4, Tensor4, ctypes.POINTER(PagedKVDesc), P, P, I32, I32, I32, I32, I32,
             I32, F, Tensor4, P, P]
-        if lib.ws_abi_version() != 2:
+        lib.ws_block_causal_attn_fwd_text.restype = ctypes.c_int
+        lib.ws_block_causal_attn_fwd_text.argtypes = [
+            Tensor4, Tensor4, Tensor4, ctypes.POINTER(PagedKVDesc), P, P, P, P, I32, I32, I32, F, I32,
+            Tensor4, P, P, ctypes.c_size_t, P]
+        lib.ws_block_causal_prefill_text.restype = ctypes.c_int
+        lib.ws_block_causal_prefill_text.argtypes = [
+            Tensor4, Tensor4, Tensor4, ctypes.POINTER(PagedKVDesc), P, P, P, P, I32, I32, I32, I32, I32,
+            I32, F, Tensor4, P, P]
+        if lib.ws_abi_version() != 3:
             raise RuntimeError("libwsattn.so ABI version mismatch")
         _LIB = lib
     return _LIB
@@ -197,11 +207,29 @@ def kv_append(cache, cache_lens, k_new, v_new):
                                   k_new.shape[1], _t4(k_new), _t4(v_new), _stream()))
 
 
+def _int32_pair(x, shape, device):
+    """(host, device) int32 tensors of the given shape from an array-like or
+    a (host, device) pair."""
+    if isinstance(x, tuple):
+        host, dev = x
+    else:
+        host = torch.as_tensor(x, dtype=torch.int32).cpu().contiguous()
+        dev = host.to(device)
+    host = host.reshape(shape)
+    dev = dev.reshape(shape)
+    if host.dtype != torch.int32 or dev.dtype != torch.int32 or not host.is_contiguous() or not dev.is_contiguous():
+        raise ValueError("int32 contiguous arrays expected")
+    return host, dev
+
+
 def block_causal_attn_fwd(q, k_new, v_new, cache, cache_lens, scale=None, fuse_append=False,
                           out=None, out_dtype=torch.bfloat16, want_lse=False, lse=None,
-                          workspace=None):
+                          workspace=None, text_starts=None):
     """One streaming step: q [B][Lq][Hq][d] of the new block attends to
     cache tokens [0, cache_lens[b]) and to its own block (k_new/v_new).
+    text_starts (optional, [B]): the new block ends in a token-causal segment
+    starting at that token of the block; new token t then sees new tokens
+    [0, max(text_starts[b], t + 1)).
     Returns out (and lse [B][Hq][Lq] f32 when want_lse)."""
     B, Lq, Hq, D = q.shape
     host, dev = _lens(cache_lens, q.device)
@@ -226,18 +254,29 @@ def block_causal_attn_fwd(q, k_new, v_new, cache, cache_lens, scale=None, fuse_a
     ws_ptr = _ptr(workspace)
     ws_len = workspace.numel() if workspace is not None else 0
     desc = cache.desc()
-    _check(library().ws_block_causal_attn_fwd(
-        _t4(q), _t4(k_new), _t4(v_new), ctypes.byref(desc), host.data_ptr(), dev.data_ptr(),
-        B, Lq, Hq, float(scale), WS_FUSE_APPEND if fuse_append else 0,
-        _t4(out), _ptr(lse), ws_ptr, ws_len, _stream()))
+    flags = WS_FUSE_APPEND if fuse_append else 0
+    if text_starts is None:
+        _check(library().ws_block_causal_attn_fwd(
+            _t4(q), _t4(k_new), _t4(v_new), ctypes.byref(desc), host.data_ptr(), dev.data_ptr(),
+            B, Lq, Hq, float(scale), flags, _t4(out), _ptr(lse), ws_ptr, ws_len, _stream()))
+    else:
+        th, td = _int32_pair(text_starts, (B,), q.device)
+        _check(library().ws_block_causal_attn_fwd_text(
+            _t4(q), _t4(k_new), _t4(v_new), ctypes.byref(desc), host.data_ptr(), dev.data_ptr(),
+            th.data_ptr(), td.data_ptr(), B, Lq, Hq, float(scale), flags, _t4(out), _ptr(lse),
+            ws_ptr, ws_len, _stream()))
     return (out, lse) if want_lse else out
 
 
 def block_causal_prefill(q, k, v, block_offsets, scale=None, cache=None, num_kv_heads=None,
-                         out=None, out_dtype=torch.bfloat16, want_lse=False, lse=None):
+                         out=None, out_dtype=torch.bfloat16, want_lse=False, lse=None,
+                         text_starts=None):
     """Whole-sequence block-causal attention.  q [B][L][Hq][d]; k, v
     [B][L][Hkv][d] or None to read them from ``cache``; block_offsets
-    [B][nb+1] (host tensor, or a (host, device) pair)."""
+    [B][nb+1] (host tensor, or a (host, device) pair).  text_starts
+    (optional, [B][nb], absolute positions): block n ends in a token-causal
+    segment starting there; its token i then sees keys
+    j < max(text_starts[b][n], i + 1)."""
     B, L, Hq, D = q.shape
     if isinstance(block_offsets, tuple):
         off_h, off_d = block_offsets
@@ -265,8 +304,14 @@ def block_causal_prefill(q, k, v, block_offsets, scale=None, cache=None, num_kv_
     if tuple(off_h.shape) != (B, nb + 1) or tuple(off_d.shape) != (B, nb + 1):
         raise ValueError("block_offsets must be [B][num_blocks + 1]")
     desc = cache.desc() if cache is not None else None
-    _check(library().ws_block_causal_prefill(
-        _t4(q), _t4(k), _t4(v), ctypes.byref(desc) if desc is not None else None,
-        off_h.data_ptr(), off_d.data_ptr(), B, L, nb, Hq, hkv, D, float(scale),
-        _t4(out), _ptr(lse), _stream()))
+    kvp = ctypes.byref(desc) if desc is not None else None
+    if text_starts is None:
+        _check(library().ws_block_causal_prefill(
+            _t4(q), _t4(k), _t4(v), kvp, off_h.data_ptr(), off_d.data_ptr(), B, L, nb, Hq, hkv, D,
+            float(scale), _t4(out), _ptr(lse), _stream()))
+    else:
+        th, td = _int32_pair(text_starts, (B, nb), q.device)
+        _check(library().ws_block_causal_prefill_text(
+            _t4(q), _t4(k), _t4(v), kvp, off_h.data_ptr(), off_d.data_ptr(), th.data_ptr(), td.data_ptr(),
+            B, L, nb, Hq, hkv, D, float(scale), _t4(out), _ptr(lse), _stream()))
     return (out, lse) if want_lse else out

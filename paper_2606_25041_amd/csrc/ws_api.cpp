@@ -164,6 +164,19 @@ bool finish_work(ws::AttnArgs &a) {
     return true;
 }
 
+int step_impl(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_kv *kv,
+              const int32_t *cache_lens_host, const int32_t *cache_lens_dev,
+              const int32_t *text_host, const int32_t *text_dev, int32_t batch,
+              int32_t new_len, int32_t num_q_heads, float scale, int32_t flags,
+              ws_tensor4 out, float *lse, void *workspace, size_t workspace_bytes,
+              void *stream);
+int prefill_impl(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, const ws_paged_kv *kv_or_null,
+                 const int32_t *block_offsets_host, const int32_t *block_offsets_dev,
+                 const int32_t *text_host, const int32_t *text_dev,
+                 int32_t batch, int32_t seq_len, int32_t num_blocks, int32_t num_q_heads,
+                 int32_t num_kv_heads, int32_t head_dim, float scale, ws_tensor4 out,
+                 float *lse, void *stream);
+
 }  // namespace
 
 extern "C" {
@@ -233,6 +246,53 @@ int ws_block_causal_attn_fwd(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, c
                              int32_t new_len, int32_t num_q_heads, float scale, int32_t flags,
                              ws_tensor4 out, float *lse, void *workspace, size_t workspace_bytes,
                              void *stream) {
+    return step_impl(q, k_new, v_new, kv, cache_lens_host, cache_lens_dev, nullptr, nullptr, batch, new_len,
+                     num_q_heads, scale, flags, out, lse, workspace, workspace_bytes, stream);
+}
+
+int ws_block_causal_attn_fwd_text(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_kv *kv,
+                                  const int32_t *cache_lens_host, const int32_t *cache_lens_dev,
+                                  const int32_t *text_starts_host, const int32_t *text_starts_dev,
+                                  int32_t batch, int32_t new_len, int32_t num_q_heads, float scale, int32_t flags,
+                                  ws_tensor4 out, float *lse, void *workspace, size_t workspace_bytes,
+                                  void *stream) {
+    if (!text_starts_host || !text_starts_dev) return fail(WS_ERR_NULL, "text_starts pointer is NULL");
+    return step_impl(q, k_new, v_new, kv, cache_lens_host, cache_lens_dev, text_starts_host, text_starts_dev,
+                     batch, new_len, num_q_heads, scale, flags, out, lse, workspace, workspace_bytes, stream);
+}
+
+int ws_block_causal_prefill(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, const ws_paged_kv *kv_or_null,
+                            const int32_t *block_offsets_host, const int32_t *block_offsets_dev,
+                            int32_t batch, int32_t seq_len, int32_t num_blocks, int32_t num_q_heads,
+                            int32_t num_kv_heads, int32_t head_dim, float scale, ws_tensor4 out,
+                            float *lse, void *stream) {
+    return prefill_impl(q, k, v, kv_or_null, block_offsets_host, block_offsets_dev, nullptr, nullptr, batch,
+                        seq_len, num_blocks, num_q_heads, num_kv_heads, head_dim, scale, out, lse, stream);
+}
+
+int ws_block_causal_prefill_text(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, const ws_paged_kv *kv_or_null,
+                                 const int32_t *block_offsets_host, const int32_t *block_offsets_dev,
+                                 const int32_t *text_starts_host, const int32_t *text_starts_dev,
+                                 int32_t batch, int32_t seq_len, int32_t num_blocks, int32_t num_q_heads,
+                                 int32_t num_kv_heads, int32_t head_dim, float scale, ws_tensor4 out,
+                                 float *lse, void *stream) {
+    if (!text_starts_host || !text_starts_dev) return fail(WS_ERR_NULL, "text_starts pointer is NULL");
+    return prefill_impl(q, k, v, kv_or_null, block_offsets_host, block_offsets_dev, text_starts_host,
+                        text_starts_dev, batch, seq_len, num_blocks, num_q_heads, num_kv_heads, head_dim,
+                        scale, out, lse, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// One streaming step (text_* NULL: no token-causal segment).
+int step_impl(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_kv *kv,
+              const int32_t *cache_lens_host, const int32_t *cache_lens_dev,
+              const int32_t *text_host, const int32_t *text_dev, int32_t batch,
+              int32_t new_len, int32_t num_q_heads, float scale, int32_t flags,
+              ws_tensor4 out, float *lse, void *workspace, size_t workspace_bytes,
+              void *stream) {
     if (int rc = check_paged(kv)) return rc;
     if (!cache_lens_host || !cache_lens_dev) return fail(WS_ERR_NULL, "cache_lens pointer is NULL");
     if (batch < 0 || new_len < 0 || num_q_heads <= 0)
@@ -257,6 +317,11 @@ int ws_block_causal_attn_fwd(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, c
         if ((int64_t)cache_lens_host[b] + new_len > max_k) max_k = (int64_t)cache_lens_host[b] + new_len;
     }
     if (max_k > INT32_MAX) return fail(WS_ERR_SHAPE, "too many keys");
+    if (text_host)
+        for (int b = 0; b < batch; ++b)
+            if (text_host[b] < 0 || text_host[b] > new_len)
+                return fail(WS_ERR_OFFSETS, "text_starts[%d] = %d outside [0, new_len %d]", b, (int)text_host[b],
+                            (int)new_len);
     if ((int64_t)(num_q_heads / kv->num_kv_heads) * new_len > WS_MAX_STEP_ROWS)
         return fail(WS_ERR_SHAPE, "new_len x query heads per KV head exceeds %lld", (long long)WS_MAX_STEP_ROWS);
     const StepPlan plan = plan_step(batch, num_q_heads, kv->num_kv_heads, new_len, max_k);
@@ -288,9 +353,16 @@ int ws_block_causal_attn_fwd(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, c
         a.part_o = (float *)workspace;
         a.part_ml = a.part_o + (size_t)plan.nsplit * batch * a.Hkv * a.nrb * 32 * kv->head_dim;
     }
+    if (text_host) {
+        a.text_starts = text_dev;
+        a.has_text = 1;
+    }
     if (batch <= ws::LENS_IN_ARGS) {
         a.lens_in_args = 1;
-        for (int b = 0; b < batch; ++b) a.lens_arg[b] = cache_lens_host[b];
+        for (int b = 0; b < batch; ++b) {
+            a.lens_arg[b] = cache_lens_host[b];
+            a.text_arg[b] = text_host ? text_host[b] : new_len;
+        }
     }
     if (!finish_work(a)) return fail(WS_ERR_SHAPE, "too many work items");
     if (int e = ws::launch_attention(a, kv->head_dim, plan.shape, stream))
@@ -301,11 +373,13 @@ int ws_block_causal_attn_fwd(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, c
     return ok();
 }
 
-int ws_block_causal_prefill(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, const ws_paged_kv *kv_or_null,
-                            const int32_t *block_offsets_host, const int32_t *block_offsets_dev,
-                            int32_t batch, int32_t seq_len, int32_t num_blocks, int32_t num_q_heads,
-                            int32_t num_kv_heads, int32_t head_dim, float scale, ws_tensor4 out,
-                            float *lse, void *stream) {
+// Whole-sequence prefill (text_* NULL: no token-causal segments).
+int prefill_impl(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, const ws_paged_kv *kv_or_null,
+                 const int32_t *block_offsets_host, const int32_t *block_offsets_dev,
+                 const int32_t *text_host, const int32_t *text_dev,
+                 int32_t batch, int32_t seq_len, int32_t num_blocks, int32_t num_q_heads,
+                 int32_t num_kv_heads, int32_t head_dim, float scale, ws_tensor4 out,
+                 float *lse, void *stream) {
     if (batch < 0 || seq_len < 0 || num_blocks < 0 || num_q_heads <= 0 || num_kv_heads <= 0)
         return fail(WS_ERR_SHAPE, "batch %d, seq_len %d, num_blocks %d, heads %d/%d", (int)batch, (int)seq_len,
                     (int)num_blocks, (int)num_q_heads, (int)num_kv_heads);
@@ -333,9 +407,16 @@ int ws_block_causal_prefill(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, const ws_p
     for (int b = 0; b < batch; ++b) {
         const int32_t *off = block_offsets_host + (int64_t)b * (num_blocks + 1);
         if (off[0] != 0) return fail(WS_ERR_OFFSETS, "block_offsets[%d][0] = %d, must be 0", b, (int)off[0]);
-        for (int n = 0; n < num_blocks; ++n)
+        for (int n = 0; n < num_blocks; ++n) {
             if (off[n + 1] < off[n])
                 return fail(WS_ERR_OFFSETS, "block_offsets[%d] decreases at %d", b, n + 1);
+            if (text_host) {
+                const int32_t t = text_host[(int64_t)b * num_blocks + n];
+                if (t < off[n] || t > off[n + 1])
+                    return fail(WS_ERR_OFFSETS, "text_starts[%d][%d] = %d outside block [%d, %d]", b, n, (int)t,
+                                (int)off[n], (int)off[n + 1]);
+            }
+        }
         if (off[num_blocks] != seq_len)
             return fail(WS_ERR_OFFSETS, "block_offsets[%d][%d] = %d, must equal seq_len %d", b, (int)num_blocks,
                         (int)off[num_blocks], (int)seq_len);
@@ -356,6 +437,10 @@ int ws_block_causal_prefill(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, const ws_p
     }
     a.offsets = block_offsets_dev;
     a.nb = num_blocks;
+    if (text_host) {
+        a.text_starts = text_dev;
+        a.has_text = 1;
+    }
     a.out = out.ptr; a.o_sb = out.stride_b; a.o_st = out.stride_t; a.o_sh = out.stride_h;
     a.out_f32 = out.dtype == WS_DTYPE_F32;
     a.lse = lse;
@@ -372,4 +457,4 @@ int ws_block_causal_prefill(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, const ws_p
     return ok();
 }
 
-}  // extern "C"
+}  // namespace

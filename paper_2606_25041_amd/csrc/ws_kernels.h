@@ -50,6 +50,11 @@ struct AttnArgs {
     const int32_t *cache_lens;
     const int32_t *offsets;
     int32_t nb;
+    // token-causal segments (has_text): step [B] starts within the new
+    // block; prefill [B][nb] absolute starts.  Token i of a block sees the
+    // keys j < max(start, i + 1) (prefill positions; step: n_pool + that).
+    const int32_t *text_starts;
+    int32_t has_text;
     // output [B][Lq][Hq][D] (bf16 or f32) and lse [B][Hq][Lq] (nullable)
     void *out;
     int64_t o_sb, o_st, o_sh;
@@ -83,10 +88,12 @@ struct AttnArgs {
     FastDiv fd_group, fd_qt, fd_g, fd_hkv, fd_split;
     FastDiv fd_gq;       // divider by G (packed row -> token)
     float scale_log2;    // scale * log2(e)
-    // step: cache lengths also passed by value when batch <= LENS_IN_ARGS,
-    // so the first page lookup does not wait on a load of them
+    // step: cache lengths (and segment starts) also passed by value when
+    // batch <= LENS_IN_ARGS, so the first page lookup does not wait on a load
+    // of them
     int32_t lens_in_args;
     int32_t lens_arg[32];
+    int32_t text_arg[32];   // step: segment starts by value (new_len: none)
 };
 
 constexpr int LENS_IN_ARGS = 32;

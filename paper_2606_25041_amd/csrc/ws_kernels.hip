@@ -81,16 +81,19 @@ __device__ __forceinline__ uint32_t fastdiv(uint32_t n, FastDiv f) {
     return (uint32_t)(((uint64_t)n * f.mul) >> f.shift);
 }
 
-// End (exclusive) of the block that holds token i: the first offset > i.
+// End (exclusive) of the keys token i of a prefill sees: the end of its
+// block (the first offset > i), or, when the block ends in a token-causal
+// segment starting at ts (text != nullptr, [nb] starts of this stream),
+// max(ts, i + 1).  Non-decreasing in i.
 template <bool UNIFORM>
-__device__ __forceinline__ int block_end(const int32_t *off, int nb, int i) {
-    auto at = [&](int k) { return UNIFORM ? ld_uniform(off, k) : off[k]; };
+__device__ __forceinline__ int row_key_end(const int32_t *off, const int32_t *text, int nb, int i) {
+    auto at = [&](const int32_t *p, int k) { return UNIFORM ? ld_uniform(p, k) : p[k]; };
     int lo = 1, hi = nb;  // answer index in [1, nb]
     while (lo < hi) {
         int mid = (lo + hi) >> 1;
-        if (at(mid) > i) hi = mid; else lo = mid + 1;
+        if (at(off, mid) > i) hi = mid; else lo = mid + 1;
     }
-    return at(lo);
+    return text ? max(at(text, lo - 1), i + 1) : at(off, lo);
 }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -242,17 +245,25 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     }
 
     // ---- key range ------------------------------------------------------
+    // Every row sees a prefix [0, kend) of the keys, and kend does not
+    // decrease along the rows of a tile, so the tile's first and last rows
+    // give the keys all rows see (kfull) and the keys any row sees (k_hi).
     const int32_t *offs = step ? nullptr : a.offsets + (int64_t)b * (a.nb + 1);
-    int n_pool, k_hi, kfull;
+    const int32_t *text = (!step && a.has_text) ? a.text_starts + (int64_t)b * a.nb : nullptr;
+    int n_pool, k_hi, kfull, ts = 0;
     if (step) {
         n_pool = !a.lens_in_args ? ld_uniform(a.cache_lens, b) : b == 0 ? (int)lens0 : a.lens_arg[b];
-        k_hi = n_pool + a.Lq;
-        kfull = k_hi;
+        // start of the new block's token-causal segment (Lq: none); new
+        // token t sees n_pool + max(ts, t + 1) keys
+        ts = a.lens_in_args ? a.text_arg[b] : a.has_text ? ld_uniform(a.text_starts, b) : a.Lq;
+        const int t_last = (int)fastdiv((uint32_t)(min(q0 + QT, (int)nrows) - 1), fd_gq);
+        k_hi = n_pool + max(ts, t_last + 1);
+        kfull = n_pool + max(ts, (int)fastdiv((uint32_t)q0, fd_gq) + 1);
     } else {
         n_pool = a.paged ? a.Lq : 0;
         const int q_last = min(q0 + QT, a.Lq) - 1;
-        k_hi = block_end<true>(offs, a.nb, q_last);
-        kfull = block_end<true>(offs, a.nb, q0);
+        k_hi = row_key_end<true>(offs, text, a.nb, q_last);
+        kfull = row_key_end<true>(offs, text, a.nb, q0);
     }
     const int ntile = (k_hi + KT - 1) / KT;
     // (split * ntile < 2^31: ntile < 2^25 and split < MAX_SPLITS = 32)
@@ -283,7 +294,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
         const int pc = min(row[n], (int)nrows - 1);
         tok[n] = row_token(pc);
         hqr[n] = row_head(pc, tok[n]);
-        kend[n] = step ? k_hi : block_end<false>(offs, a.nb, tok[n]);
+        kend[n] = step ? n_pool + max(ts, tok[n] + 1) : row_key_end<false>(offs, text, a.nb, tok[n]);
     }
 
     // ---- direct-to-LDS tile loads -----------------------------------------
@@ -517,8 +528,10 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
             const float mx = halves_max(mx_lane[n]) * c2;
             const bool grow = mx > m[n] + RESCALE_LOG2;
             if (__builtin_amdgcn_ballot_w64(grow)) {
+                // lanes that keep m scale by 1 (also while m is still -inf:
+                // a row that sees no key of this tile); 0 from -inf
                 const float m_new = grow ? mx : m[n];
-                const float alpha = fast_exp2(m[n] - m_new);  // 1 where m is kept; 0 from -inf
+                const float alpha = grow ? fast_exp2(m[n] - m_new) : 1.f;
                 m[n] = m_new;
                 l[n] *= alpha;
 #pragma unroll

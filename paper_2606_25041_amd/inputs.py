@@ -42,14 +42,29 @@ def bf16_bits(t):
     return t.contiguous().view(torch.int16).numpy().view(np.uint16)
 
 
-def interleaved_block_lengths(g, nblocks):
-    """Per-unit token counts of an interleaved stream: a 4-frame visual
-    segment of U{64..256} tokens in total, an audio segment of U{4..16} and a
-    text segment of U{0..8} (inclusive bounds)."""
+def interleaved_segments(g, nblocks):
+    """Per-unit segment token counts of an interleaved stream, in block order
+    [visual, audio, text]: a 4-frame visual segment of U{64..256} tokens in
+    total, an audio segment of U{4..16} and a text segment of U{0..8}
+    (inclusive bounds).  Returns (vis, aud, txt) int64 arrays."""
     vis = g.integers(64, 257, size=nblocks)
     aud = g.integers(4, 17, size=nblocks)
     txt = g.integers(0, 9, size=nblocks)
-    return (vis + aud + txt).astype(np.int64)
+    return vis.astype(np.int64), aud.astype(np.int64), txt.astype(np.int64)
+
+
+def interleaved_block_lengths(g, nblocks):
+    """Per-unit token counts of an interleaved stream (sum of the segments of
+    ``interleaved_segments``)."""
+    vis, aud, txt = interleaved_segments(g, nblocks)
+    return vis + aud + txt
+
+
+def text_starts_of(offsets, text_lens):
+    """Absolute start of each block's trailing text segment: [B][nb] from
+    block offsets [B][nb+1] and per-block text lengths [B][nb]."""
+    offsets = np.asarray(offsets, dtype=np.int64)
+    return (offsets[:, 1:] - np.asarray(text_lens, dtype=np.int64)).astype(np.int32)
 
 
 def interleaved_block_lengths_per_frame(g, nblocks):
@@ -91,6 +106,9 @@ class Workload:
     out_f32: bool = False
     fuse_append: bool = False
     seed: int = 0
+    # token-causal segments: prefill [B][nb] absolute starts; step [B]
+    # starts within the new block (None: plain block-causal)
+    text_starts: Optional[np.ndarray] = None
 
     # step views: the cache part and the new block of the logical K/V
     @property
@@ -168,6 +186,28 @@ def config(idx, seed=None, c4_reading="B"):
         return step_workload("streams_b4_gqa64x8_d128_q512_c131072", 4, 64, 8, 128, 512, [131072] * 4,
                              seed, fuse_append=True)
     raise ValueError(f"no workload {idx}")
+
+
+def thinker_prefill(seed=1006, nblocks=128):
+    """The interleaved workload (1 stream, GQA 40/8 x 128, 128 variable
+    blocks, paged) with each block's text segment token-causal: the
+    thinker's pass over the language and state slots."""
+    g = rng(seed, S_LENGTHS)
+    vis, aud, txt = interleaved_segments(g, nblocks)
+    wl = prefill_workload(f"thinker_prefill_b1_gqa40x8_d128_{nblocks}blk_{int((vis + aud + txt).sum())}tok",
+                          1, 40, 8, 128, [vis + aud + txt], seed, paged=True)
+    wl.text_starts = text_starts_of(wl.offsets, txt[None])
+    return wl
+
+
+def thinker_step(B=4, Hq=64, Hkv=8, Lq=8, Lc=131072, seed=1007):
+    """A token-causal decode step of the thinker: B streams append Lq
+    language/state tokens, all token-causal (segment start 0), to caches of
+    Lc tokens (GQA Hq/Hkv x 128), committed in the same launch."""
+    wl = step_workload(f"thinker_step_b{B}_gqa{Hq}x{Hkv}_d128_q{Lq}_c{Lc}", B, Hq, Hkv, 128, Lq,
+                       [Lc] * B, seed, fuse_append=True)
+    wl.text_starts = np.zeros(B, np.int32)
+    return wl
 
 
 def sample_rows(g, B, Hq, L, n, must=()):

@@ -76,23 +76,25 @@ def run_gpu(wl, cache=None, out_dtype=None, want_lse=True, fuse=None):
     if wl.kind == "prefill":
         if wl.paged:
             return ws.block_causal_prefill(q, None, None, wl.offsets, scale=wl.scale, cache=cache,
-                                           num_kv_heads=wl.Hkv, out_dtype=out_dtype, want_lse=want_lse)
+                                           num_kv_heads=wl.Hkv, out_dtype=out_dtype, want_lse=want_lse,
+                                           text_starts=wl.text_starts)
         return ws.block_causal_prefill(q, to_dev_bf16(wl.k), to_dev_bf16(wl.v), wl.offsets,
-                                       scale=wl.scale, out_dtype=out_dtype, want_lse=want_lse)
+                                       scale=wl.scale, out_dtype=out_dtype, want_lse=want_lse,
+                                       text_starts=wl.text_starts)
     fuse = wl.fuse_append if fuse is None else fuse
     return ws.block_causal_attn_fwd(q, to_dev_bf16(wl.k_new), to_dev_bf16(wl.v_new), cache,
                                     wl.cache_lens, scale=wl.scale, fuse_append=fuse,
-                                    out_dtype=out_dtype, want_lse=want_lse)
+                                    out_dtype=out_dtype, want_lse=want_lse, text_starts=wl.text_starts)
 
 
 def run_oracle(wl, rows=None):
     """fp64 oracle on the same bf16 inputs.  rows: optional (b, h, i) list."""
     if wl.kind == "prefill":
         return oracle.prefill(inputs.bf16_bits(wl.q), inputs.bf16_bits(wl.k), inputs.bf16_bits(wl.v),
-                              wl.offsets, wl.scale, rows=rows)
+                              wl.offsets, wl.scale, rows=rows, text_starts=wl.text_starts)
     return oracle.step(inputs.bf16_bits(wl.q), inputs.bf16_bits(wl.k_cache), inputs.bf16_bits(wl.v_cache),
                        wl.cache_lens, inputs.bf16_bits(wl.k_new), inputs.bf16_bits(wl.v_new), wl.scale,
-                       rows=rows)
+                       rows=rows, text_starts=wl.text_starts)
 
 
 def compare(out, lse, ref_out, ref_lse, rows=None):

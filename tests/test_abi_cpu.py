@@ -41,10 +41,11 @@ def header_functions():
 def test_exports_every_declared_symbol(lib):
     names = header_functions()
     assert {"ws_kv_append", "ws_block_causal_attn_fwd", "ws_block_causal_prefill",
+            "ws_block_causal_attn_fwd_text", "ws_block_causal_prefill_text",
             "ws_workspace_bytes", "ws_abi_version", "ws_status_string", "ws_last_error"} <= set(names)
     for name in names:
         assert hasattr(lib, name), name
-    assert lib.ws_abi_version() == 2
+    assert lib.ws_abi_version() == 3
     assert lib.ws_status_string(0) == b"WS_OK"
     assert lib.ws_status_string(10) == b"WS_ERR_HIP"
 
@@ -182,6 +183,47 @@ def test_prefill_errors(lib):
     h.table[0, 2] = 77
     assert prefill_call(lib, [[0, 150]], k=null, v=null, desc=h.desc()) == 6
     assert prefill_call(lib, [[0, 150]], k=null, v=null, desc=h.desc(num_kv_heads=4)) == 8
+
+
+def step_text_call(lib, h, starts, B=2, Lq=16, Hq=4, lse=None, starts_dev=FAKE):
+    desc = h.desc()
+    st = np.ascontiguousarray(np.asarray(starts, np.int32)) if starts is not None else None
+    return lib.ws_block_causal_attn_fwd_text(t4(H=Hq, L=Lq), t4(H=2, L=Lq), t4(H=2, L=Lq), ctypes.byref(desc),
+                                             h.lens.ctypes.data, FAKE,
+                                             st.ctypes.data if st is not None else None, starts_dev,
+                                             B, Lq, Hq, 0.088, 0, t4(H=Hq, L=Lq), lse, FAKE, 1 << 30, None)
+
+
+def test_step_text_errors(lib):
+    h = Host()
+    assert step_text_call(lib, h, None) == 1                  # NULL host starts
+    assert step_text_call(lib, h, [0, 3], starts_dev=None) == 1
+    assert step_text_call(lib, h, [0, 17]) == 5               # start past new_len (16)
+    assert step_text_call(lib, h, [-1, 3]) == 5
+    # valid starts (0 and new_len) pass to the next check: a misaligned lse
+    assert step_text_call(lib, h, [0, 16], lse=FAKE + 2) == 4
+
+
+def prefill_text_call(lib, offs, starts, B=1, starts_dev=FAKE, lse=None):
+    offs = np.ascontiguousarray(np.asarray(offs, np.int32))
+    L = int(offs.reshape(B, -1)[0, -1])
+    nb = offs.reshape(B, -1).shape[1] - 1
+    st = np.ascontiguousarray(np.asarray(starts, np.int32)) if starts is not None else None
+    return lib.ws_block_causal_prefill_text(t4(H=4, L=L), t4(H=2, L=L), t4(H=2, L=L), None,
+                                            offs.ctypes.data, FAKE, st.ctypes.data if st is not None else None,
+                                            starts_dev, B, L, nb, 4, 2, 128, 0.1, t4(H=4, L=L), lse, None)
+
+
+def test_prefill_text_errors(lib):
+    assert prefill_text_call(lib, [[0, 5, 9]], None) == 1
+    assert prefill_text_call(lib, [[0, 5, 9]], [[0, 5]], starts_dev=None) == 1
+    assert prefill_text_call(lib, [[0, 5, 9]], [[6, 7]]) == 5     # start past its block's end
+    assert prefill_text_call(lib, [[0, 5, 9]], [[0, 4]]) == 5     # start before its block
+    assert prefill_text_call(lib, [[0, 5, 5, 9]], [[2, 6, 9]]) == 5   # empty block: start must be 5
+    assert prefill_text_call(lib, [[0, 4, 8], [0, 2, 8]], [[1, 8], [2, 9]], B=2) == 5
+    # starts at the block bounds are valid: the call reaches a later check
+    assert prefill_text_call(lib, [[0, 5, 5, 9]], [[5, 5, 5]], lse=FAKE + 2) == 4
+    assert prefill_text_call(lib, [[0, 5, 9]], [[0, 9]], lse=FAKE + 2) == 4
 
 
 def test_empty_calls_are_ok(lib):

@@ -1,0 +1,174 @@
+"""GPU parity of token-causal segments (the thinker's language and state
+slots, decoded token by token: Sec. 1 and Sec. 2.4): blocks whose tail is
+causal token by token, through the *_text entry points, against the fp64
+oracle.  Tolerance as for the block-causal path: max-abs 2e-2, mean-abs
+2e-3 (bf16 outputs), lse 1e-3."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2606_25041_amd as ws
+from paper_2606_25041_amd import inputs
+from tests import gpu_support as gs
+
+pytestmark = pytest.mark.gpu
+
+
+def _random_prefill(name, B, Hq, Hkv, D, L, nb, seed, paged=False, out_f32=False):
+    """Ragged random blocks; each block's segment start drawn uniformly in
+    [block start, block end] (empty and whole-block segments included)."""
+    g = np.random.default_rng([seed, 98])
+    lens = []
+    for _ in range(B):
+        cuts = np.sort(g.choice(np.arange(1, L), size=nb - 1, replace=False))
+        lens.append(np.diff(np.concatenate([[0], cuts, [L]])))
+    wl = inputs.prefill_workload(name, B, Hq, Hkv, D, lens, seed, paged=paged, out_f32=out_f32)
+    off = wl.offsets.astype(np.int64)
+    wl.text_starts = np.array([[g.integers(off[b, n], off[b, n + 1] + 1) for n in range(nb)]
+                               for b in range(B)], np.int32)
+    wl.text_starts[:, 0] = off[:, 0]            # a whole-block segment
+    wl.text_starts[:, 1] = off[:, 2]            # an empty segment
+    return wl
+
+
+def _check_full(wl, cache=None, **kw):
+    gs.say(f"[gpu] {wl.name}: B={wl.B} Hq={wl.Hq} Hkv={wl.Hkv} D={wl.D} Lq={wl.Lq} text={wl.text_starts.tolist()[:1]}")
+    out, lse = gs.run_gpu(wl, cache=cache, **kw)
+    torch.cuda.synchronize()
+    ref, ref_lse = gs.run_oracle(wl)
+    stats = gs.compare(out, lse, ref, ref_lse)
+    gs.assert_close(stats)
+    return out, lse
+
+
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("L,nb", [(777, 9), (1300, 40)])
+def test_prefill_text_contiguous(D, L, nb):
+    _check_full(_random_prefill(f"text_prefill_d{D}_L{L}", 2, 4, 2, D, L, nb, seed=51 + L + D))
+
+
+def test_prefill_text_paged_interleaved_f32():
+    """Interleaved units [visual, audio, text] with the text segment causal,
+    read from a shuffled paged cache, f32 output."""
+    g = inputs.rng(53, inputs.S_LENGTHS)
+    vis, aud, txt = inputs.interleaved_segments(g, 10)
+    wl = inputs.prefill_workload("text_prefill_paged", 1, 5, 1, 128, [vis + aud + txt], 53, paged=True,
+                                 out_f32=True)
+    wl.text_starts = inputs.text_starts_of(wl.offsets, txt[None])
+    cache = gs.device_cache(wl, [wl.Lq])
+    _check_full(wl, cache=cache)
+
+
+def test_prefill_all_text_is_causal():
+    """Every block token-causal: standard causal attention over 700 tokens
+    in 5 blocks (the oracle pin shows the same identity on the CPU)."""
+    lens = [np.array([1, 300, 64, 35, 300])]
+    wl = inputs.prefill_workload("text_all_causal", 1, 2, 1, 128, lens, 55)
+    wl.text_starts = wl.offsets[:, :-1].copy()
+    _check_full(wl)
+
+
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("Lq,lens,starts", [(100, [0, 333, 64], [0, 37, 100]),
+                                            (300, [129, 0, 1000], [299, 0, 150])])
+def test_step_text_ragged(D, Lq, lens, starts):
+    wl = inputs.step_workload(f"text_step_d{D}_q{Lq}", 3, 8, 2, D, Lq, lens, seed=57 + Lq + D)
+    wl.text_starts = np.array(starts, np.int32)
+    cache = gs.device_cache(wl, wl.cache_lens)
+    _check_full(wl, cache=cache)
+
+
+@pytest.mark.parametrize("out_dtype", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("Lq", [1, 4, 8, 37])
+def test_step_token_causal_decode_gqa8(Lq, out_dtype):
+    """Tiny token-causal blocks of a GQA-8 model over split caches: the last
+    splits hold keys the early tokens of the block may not see, so some rows
+    see no key of a whole split."""
+    wl = inputs.step_workload(f"text_decode_gqa8_q{Lq}", 2, 16, 2, 128, Lq, [4100, 2500], seed=59 + Lq)
+    wl.text_starts = np.zeros(2, np.int32)
+    cache = gs.device_cache(wl, wl.cache_lens)
+    _check_full(wl, cache=cache, out_dtype=out_dtype)
+
+
+def test_step_text_many_streams_from_memory():
+    """More than 32 streams: the segment starts are read from the device."""
+    g = np.random.default_rng(61)
+    lens = [int(x) for x in g.integers(0, 700, size=40)]
+    wl = inputs.step_workload("text_step_b40", 40, 2, 1, 64, 8, lens, seed=61)
+    wl.text_starts = g.integers(0, 9, size=40).astype(np.int32)
+    cache = gs.device_cache(wl, wl.cache_lens)
+    _check_full(wl, cache=cache)
+
+
+def test_empty_segments_match_block_causal_bitwise():
+    """Segments that start at the block end: bitwise the plain entry points."""
+    wl = _random_prefill("text_empty", 2, 4, 2, 128, 900, 7, seed=63)
+    wl.text_starts = wl.offsets[:, 1:].copy()
+    a, la = gs.run_gpu(wl)
+    wl.text_starts = None
+    b, lb = gs.run_gpu(wl)
+    st = inputs.step_workload("text_empty_step", 2, 8, 2, 128, 40, [3000, 77], seed=64)
+    cache = gs.device_cache(st, st.cache_lens)
+    c, lc = gs.run_gpu(st, cache=cache)
+    st.text_starts = np.full(2, 40, np.int32)
+    d, ld = gs.run_gpu(st, cache=cache)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b) and torch.equal(la, lb)
+    assert torch.equal(c, d) and torch.equal(lc, ld)
+
+
+def test_streaming_replay_equals_prefill_text():
+    """Block by block (step with the block's segment start, then commit)
+    reproduces the token-causal prefill rows of every block."""
+    g = inputs.rng(65, inputs.S_LENGTHS)
+    vis, aud, txt = inputs.interleaved_segments(g, 6)
+    wl = inputs.prefill_workload("text_replay", 1, 4, 2, 128, [vis + aud + txt], 65, paged=True)
+    wl.text_starts = inputs.text_starts_of(wl.offsets, txt[None])
+    cache = gs.device_cache(wl, [wl.Lq])
+    gs.say("[gpu] token-causal streaming replay vs prefill")
+    full, full_lse = gs.run_gpu(wl, cache=cache)
+    sc = ws.PagedCache.allocate(wl.num_pages, wl.Hkv, wl.D, torch.from_numpy(wl.page_table),
+                                device=gs.dev(), fill_bits=gs.NAN_BITS)
+    q, k, v = gs.to_dev_bf16(wl.q), gs.to_dev_bf16(wl.k), gs.to_dev_bf16(wl.v)
+    offs = wl.offsets[0]
+    for j in range(len(offs) - 1):
+        s, e = int(offs[j]), int(offs[j + 1])
+        out, lse = ws.block_causal_attn_fwd(q[:, s:e], k[:, s:e], v[:, s:e], sc, [s], scale=wl.scale,
+                                            fuse_append=True, want_lse=True,
+                                            text_starts=[int(wl.text_starts[0, j]) - s])
+        err = (out.float() - full[:, s:e].float()).abs()
+        assert err.max().item() <= 2e-2 and err.mean().item() <= 2e-3, j
+        assert (lse - full_lse[:, :, s:e]).abs().max().item() <= 1e-3, j
+    torch.cuda.synchronize()
+    assert torch.equal(sc.k_pool.view(torch.int16), cache.k_pool.view(torch.int16))
+
+
+# ---------------------------------------------------------------------------
+# full-size thinker workloads (sampled rows)
+
+def test_thinker_prefill_full_size():
+    wl = inputs.thinker_prefill()
+    cache = gs.device_cache(wl, [wl.Lq], fill_on_gpu=True)
+    ts, offs = wl.text_starts[0], wl.offsets[0]
+    must = [(0, 0, int(ts[j])) for j in (0, 60, 127)] + [(0, 39, int(offs[j + 1]) - 1) for j in (1, 64, 127)]
+    must += [(0, 7, int(ts[j]) - 1) for j in (3, 90) if ts[j] > offs[j]]
+    g = np.random.default_rng(5)
+    rows = inputs.sample_rows(g, wl.B, wl.Hq, wl.Lq, 40, must=must)
+    gs.say(f"[gpu] {wl.name}: full size, {len(rows)} sampled rows")
+    out, lse = gs.run_gpu(wl, cache=cache)
+    torch.cuda.synchronize()
+    ref, ref_lse = gs.run_oracle(wl, rows=rows)
+    gs.assert_close(gs.compare(out, lse, ref, ref_lse, rows=rows))
+    assert torch.isfinite(out).all()
+
+
+def test_thinker_decode_step_full_size():
+    wl = inputs.thinker_step()
+    cache = gs.device_cache(wl, wl.cache_lens, fill_on_gpu=True)
+    rows = [(b, h, t) for b in range(wl.B) for h in (0, 9, 63) for t in (0, 3, 7)]
+    gs.say(f"[gpu] {wl.name}: full size, {len(rows)} sampled rows")
+    out, lse = gs.run_gpu(wl, cache=cache)
+    torch.cuda.synchronize()
+    ref, ref_lse = gs.run_oracle(wl, rows=np.array(rows, np.int32))
+    gs.assert_close(gs.compare(out, lse, ref, ref_lse, rows=np.array(rows, np.int32)))
+    assert torch.isfinite(out).all()
