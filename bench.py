@@ -56,13 +56,29 @@ def kernel_source_hash():
 # algorithmic work of a workload
 
 def visible_pairs(wl):
-    """Visible (query, key) pairs per (stream, query head)."""
+    """Visible (query, key) pairs per (stream, query head).  With token-causal
+    segments (text_starts), token i of a block with segment start ts sees
+    max(ts, i + 1) keys (step: after the stream's cache)."""
+    ts_all = getattr(wl, "text_starts", None)
     if wl.kind == "step":
-        return [int(wl.Lq) * (int(c) + int(wl.Lq)) for c in wl.cache_lens]
+        out = []
+        for b, c in enumerate(wl.cache_lens):
+            lq = int(wl.Lq)
+            ts = lq if ts_all is None else int(ts_all[b])
+            # sum over t < lq of max(ts, t + 1)
+            own = ts * ts + (lq * (lq + 1) - ts * (ts + 1)) // 2
+            out.append(lq * int(c) + own)
+        return out
     out = []
-    for off in wl.offsets:
-        lens = np.diff(off.astype(np.int64))
-        out.append(int(np.sum(lens * off[1:].astype(np.int64))))
+    for b, off in enumerate(wl.offsets):
+        off = off.astype(np.int64)
+        s, e = off[:-1], off[1:]
+        if ts_all is None:
+            out.append(int(np.sum((e - s) * e)))
+        else:
+            t = np.asarray(ts_all[b], dtype=np.int64)
+            # rows [s, t) see t keys; rows i in [t, e) see i + 1
+            out.append(int(np.sum((t - s) * t + (e * (e + 1) - t * (t + 1)) // 2)))
     return out
 
 
@@ -105,6 +121,10 @@ class DeviceCase:
                                                 fill_bits=0x7FC1)
             lens = torch.from_numpy(wl.cache_lens.astype(np.int32))
             self.lens = (lens, lens.to(dev))
+            self.text = None
+            if wl.text_starts is not None:
+                th = torch.from_numpy(np.ascontiguousarray(wl.text_starts, dtype=np.int32))
+                self.text = (th, th.to(dev))
             kc = wl.k_cache.contiguous().to(dev)
             vc = wl.v_cache.contiguous().to(dev)
             n = int(wl.cache_lens.min())
@@ -118,6 +138,10 @@ class DeviceCase:
         else:
             off = torch.from_numpy(wl.offsets.astype(np.int32))
             self.offsets = (off, off.to(dev))
+            self.text = None
+            if wl.text_starts is not None:
+                th = torch.from_numpy(np.ascontiguousarray(wl.text_starts, dtype=np.int32))
+                self.text = (th, th.to(dev))
             if wl.paged:
                 self.cache = ws.PagedCache.allocate(wl.num_pages, wl.Hkv, wl.D,
                                                     torch.from_numpy(wl.page_table), device=dev,
@@ -136,11 +160,12 @@ class DeviceCase:
         if wl.kind == "step":
             ws.block_causal_attn_fwd(self.q, self.k_new, self.v_new, self.cache, self.lens,
                                      scale=wl.scale, fuse_append=wl.fuse_append, out=self.out,
-                                     lse=self.lse, want_lse=True, workspace=self.workspace)
+                                     lse=self.lse, want_lse=True, workspace=self.workspace,
+                                     text_starts=self.text)
         else:
             ws.block_causal_prefill(self.q, self.k, self.v, self.offsets, scale=wl.scale,
                                     cache=self.cache, num_kv_heads=wl.Hkv, out=self.out,
-                                    lse=self.lse, want_lse=True)
+                                    lse=self.lse, want_lse=True, text_starts=self.text)
 
 
 def time_workload(wl, steps, warmup, dev, rotate=True, latency_steps=None):
@@ -196,16 +221,19 @@ class SweepPoint:
     out_f32 = False
     fuse_append = True
 
-    def __init__(self, sweep, B, Hq, Hkv, Lq, Lc):
+    def __init__(self, sweep, B, Hq, Hkv, Lq, Lc, token_causal=False):
         self.sweep, self.B, self.Hq, self.Hkv, self.Lq, self.Lc = sweep, B, Hq, Hkv, Lq, Lc
         self.cache_lens = np.full(B, Lc, dtype=np.int64)
-        self.name = f"{sweep}_b{B}_h{Hq}x{Hkv}_q{Lq}_c{Lc}"
+        # token-causal block (segment start 0): the thinker's decode step
+        self.text_starts = np.zeros(B, np.int32) if token_causal else None
+        self.name = f"{sweep}_b{B}_h{Hq}x{Hkv}_q{Lq}_c{Lc}" + ("_tokcausal" if token_causal else "")
 
 
 SWEEPS = ([SweepPoint("S1", 1, 24, 24, 256, c) for c in (0, 1024, 4096, 16384, 65536, 131072)]
           + [SweepPoint("S2", 4, 64, 8, 512, c) for c in (4096, 16384, 32768, 65536, 131072)]
           + [SweepPoint("S3", 4, 64, 8, lq, 131072) for lq in (16, 64)]
-          + [SweepPoint("S3", 1, 24, 24, lq, 131072) for lq in (16, 64)])
+          + [SweepPoint("S3", 1, 24, 24, lq, 131072) for lq in (16, 64)]
+          + [SweepPoint("S5", 4, 64, 8, lq, c, token_causal=True) for lq in (1, 4, 8) for c in (32768, 131072)])
 
 
 class SweepCase:
@@ -231,11 +259,15 @@ class SweepCase:
         self.lse = torch.empty((B, Hq, Lq), dtype=torch.float32, device=dev)
         need = ws.workspace_bytes(ws.WS_OP_STEP, B, Hq, Hkv, Lq, pt.Lc + Lq)
         self.workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+        self.text = None
+        if pt.text_starts is not None:
+            th = torch.from_numpy(pt.text_starts)
+            self.text = (th, th.to(dev))
 
     def run(self):
         ws.block_causal_attn_fwd(self.q, self.k_new, self.v_new, self.cache, self.lens,
                                  fuse_append=True, out=self.out, lse=self.lse, want_lse=True,
-                                 workspace=self.workspace)
+                                 workspace=self.workspace, text_starts=self.text)
 
 
 def run_sweeps(dev, steps):
@@ -362,10 +394,12 @@ def main():
 
     extra = []
     if not args.no_extra:
-        for idx in (3, 4, 5):
+        for idx in (3, 4, 5, "thinker"):
             if idx == args.config:
                 continue
-            w2 = inputs.config(idx)
+            # "thinker": the interleaved workload with each unit's text
+            # segment token-causal
+            w2 = inputs.thinker_prefill() if idx == "thinker" else inputs.config(idx)
             f2, b2 = algorithmic_flops(w2), algorithmic_bytes(w2)
             wms, emean, emed, _ = time_workload(w2, max(3, args.steps // 5), 2, dev, latency_steps=0)
             extra.append({"workload": w2.name, "ms": round(emean, 4), "TFLOP/s": round(f2 / (emean * 1e-3) / 1e12, 1),
