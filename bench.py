@@ -307,6 +307,66 @@ def run_sweeps(dev, steps):
     return points
 
 
+def solver_loop_timing(dev, steps=8, reps=40):
+    """The performer's loop for one streaming unit at the headline shape
+    (MHA 24 x 128, 256-token block, 4096 cached tokens, paged): ``steps`` - 1
+    solver steps of a changing noisy block against the fixed cache, then a
+    step that commits the clean block.  Timed eagerly and as one captured
+    HIP graph replay (events on the launch stream; median over ``reps``).
+    The same cache is read by every step of a unit, so after the first step
+    it is served from the 256 MB last-level cache, as in the real loop."""
+    wl = inputs.config(2)
+    case = DeviceCase(wl, dev)
+    g = torch.Generator(device=dev)
+    g.manual_seed(9100)
+    shp_q, shp_kv = tuple(case.q.shape), tuple(case.k_new.shape)
+    qs = [torch.randn(shp_q, generator=g, device=dev).to(torch.bfloat16) for _ in range(steps)]
+    ks = [torch.randn(shp_kv, generator=g, device=dev).to(torch.bfloat16) for _ in range(steps)]
+    vs = [torch.randn(shp_kv, generator=g, device=dev).to(torch.bfloat16) for _ in range(steps)]
+    outs = [torch.empty_like(case.out) for _ in range(steps)]
+
+    def loop():
+        for s in range(steps):
+            ws.block_causal_attn_fwd(qs[s], ks[s], vs[s], case.cache, case.lens, scale=wl.scale,
+                                     fuse_append=(s == steps - 1), out=outs[s], workspace=case.workspace)
+
+    def timed(fn):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b in ev:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        return float(np.median([a.elapsed_time(b) for a, b in ev]))
+
+    for _ in range(3):
+        loop()
+    torch.cuda.synchronize()
+    eager = timed(loop)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        loop()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        loop()
+    for _ in range(3):
+        graph.replay()
+    torch.cuda.synchronize()
+    replay = timed(graph.replay)
+    flops = algorithmic_flops(wl) * steps
+    log(f"[bench] solver loop x{steps}: eager {eager * 1e3:.1f} us, graph replay {replay * 1e3:.1f} us per unit")
+    out = {"workload": f"solver_loop_b1_mha24_d128_q256_c4096_x{steps}", "steps_per_unit": steps,
+           "eager_ms_per_unit": round(eager, 5), "graph_ms_per_unit": round(replay, 5),
+           "eager_TFLOP/s": round(flops / (eager * 1e-3) / 1e12, 1),
+           "graph_TFLOP/s": round(flops / (replay * 1e-3) / 1e12, 1)}
+    del case, qs, ks, vs, outs, graph
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(wl):
     """The fp64 oracle (as it stands) on the whole headline step."""
     import oracle  # test infrastructure: only this baseline leg uses it
@@ -408,6 +468,8 @@ def main():
             del w2
             torch.cuda.empty_cache()
 
+    if not args.no_extra:
+        extra.append(solver_loop_timing(dev))
     sweeps = [] if (args.no_extra or args.no_sweep) else run_sweeps(dev, 200)
     cpu = None if args.no_cpu else cpu_baseline(wl)
     line = {

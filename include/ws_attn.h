@@ -54,6 +54,13 @@
  *   across the ABI.  ws_last_error() gives a human-readable reason.
  * - Supported: head_dim 64 or 128; inputs bf16; outputs bf16 or f32;
  *   page_size 64.
+ * - The attention and append entry points enqueue kernels only (no device
+ *   allocation, no synchronisation, no memset), so a caller may record them
+ *   into a HIP graph by stream capture, e.g. the performer's solver loop of a
+ *   unit (Sec. 2.4).  A replay repeats the recorded call exactly: the host
+ *   arrays (cache lengths, page ids, offsets, segment starts) are read when
+ *   the call is recorded, and small batches pass cache lengths and segment
+ *   starts to the kernels by value.
  * - A call with no token to process (batch == 0, or new_len / seq_len == 0)
  *   returns WS_OK after checking its scalar arguments, enqueues nothing and
  *   accepts NULL tensor pointers.

@@ -1,0 +1,100 @@
+"""The performer's solver loop (Sec. 2.4: per streaming unit, several
+flow-matching solver steps of the noisy unit against the fixed full-history
+cache, then the clean unit is committed; Sec. 1 and Sec. 2.4 mention graph
+capture) recorded once into a HIP graph and replayed.  The entry points
+enqueue kernels only (no allocation, synchronisation or memset), so the
+whole loop can be captured; every replay, with eager work and
+synchronisations in between, must give bitwise the eager results."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2606_25041_amd as ws
+from paper_2606_25041_amd import inputs
+from tests import gpu_support as gs
+
+pytestmark = pytest.mark.gpu
+
+
+def _pair(a):
+    h = torch.as_tensor(np.asarray(a), dtype=torch.int32).contiguous()
+    return h, h.to(gs.dev())
+
+
+def _loop_buffers(wl, steps):
+    """Device inputs of every solver step (a fresh noisy block each step) and
+    preallocated outputs, lse and workspace."""
+    qs, ks, vs = [], [], []
+    for s in range(steps):
+        qs.append(gs.to_dev_bf16(inputs.bf16_normal(inputs.rng(700 + s, inputs.S_Q), tuple(wl.q.shape))))
+        ks.append(gs.to_dev_bf16(inputs.bf16_normal(inputs.rng(700 + s, inputs.S_K), tuple(wl.k_new.shape))))
+        vs.append(gs.to_dev_bf16(inputs.bf16_normal(inputs.rng(700 + s, inputs.S_V), tuple(wl.v_new.shape))))
+    outs = [torch.empty(tuple(wl.q.shape), dtype=torch.bfloat16, device=gs.dev()) for _ in range(steps)]
+    lses = [torch.empty((wl.B, wl.Hq, wl.Lq), dtype=torch.float32, device=gs.dev()) for _ in range(steps)]
+    need = ws.workspace_bytes(ws.WS_OP_STEP, wl.B, wl.Hq, wl.Hkv, wl.Lq, int(max(wl.cache_lens)) + wl.Lq)
+    work = torch.empty(max(need, 16), dtype=torch.uint8, device=gs.dev())
+    return qs, ks, vs, outs, lses, work
+
+
+def _run_loop(cache, lens, text, bufs):
+    """steps - 1 uncommitted solver steps, then a step that commits its block."""
+    qs, ks, vs, outs, lses, work = bufs
+    n = len(qs)
+    for s in range(n):
+        ws.block_causal_attn_fwd(qs[s], ks[s], vs[s], cache, lens, fuse_append=(s == n - 1),
+                                 out=outs[s], lse=lses[s], want_lse=True, workspace=work,
+                                 text_starts=text)
+
+
+@pytest.mark.parametrize("token_causal", [False, True], ids=["performer", "thinker"])
+def test_solver_loop_graph_replays_match_eager(token_causal):
+    B, Hq, Hkv, D, Lq, lens = 2, 8, 2, 128, 48, [700, 333]
+    wl = inputs.step_workload("graph_loop", B, Hq, Hkv, D, Lq, lens, seed=71)
+    cache = gs.device_cache(wl, wl.cache_lens)
+    k0, v0 = cache.k_pool.clone(), cache.v_pool.clone()
+    lens_p = _pair(wl.cache_lens)
+    text = _pair(np.array([0, 20])) if token_causal else None
+    bufs = _loop_buffers(wl, 4)
+    gs.say(f"[gpu] solver loop eager, token_causal={token_causal}")
+    _run_loop(cache, lens_p, text, bufs)
+    torch.cuda.synchronize()
+    ref = [o.clone() for o in bufs[3]] + [l.clone() for l in bufs[4]]
+    ref_k, ref_v = cache.k_pool.clone(), cache.v_pool.clone()
+    # the eager loop matches the oracle (the last step sees its own block)
+    wl.q = bufs[0][3].cpu()
+    wl.k[:, wl.Lc_max:] = bufs[1][3].cpu()
+    wl.v[:, wl.Lc_max:] = bufs[2][3].cpu()
+    wl.text_starts = np.array([0, 20], np.int32) if token_causal else None
+    o_ref, l_ref = gs.run_oracle(wl)
+    gs.assert_close(gs.compare(ref[3], ref[7], o_ref, l_ref))
+
+    gs.say("[gpu] capture")
+    cache.k_pool.copy_(k0)
+    cache.v_pool.copy_(v0)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):      # warm-up on a side stream before capture
+        _run_loop(cache, lens_p, text, bufs)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        _run_loop(cache, lens_p, text, bufs)
+    torch.cuda.synchronize()
+    other = inputs.prefill_workload("graph_other", 1, 4, 2, 128, [np.array([100, 60])], 72)
+    for rep in range(3):
+        gs.say(f"[gpu] replay {rep}")
+        cache.k_pool.copy_(k0)
+        cache.v_pool.copy_(v0)
+        for o in bufs[3] + bufs[4]:
+            o.fill_(7.0)
+        torch.cuda.synchronize()
+        graph.replay()
+        # eager work between replays
+        gs.run_gpu(other)
+        torch.cuda.synchronize()
+        got = bufs[3] + bufs[4]
+        for a, b in zip(got, ref):
+            assert torch.equal(a, b), rep
+        assert torch.equal(cache.k_pool.view(torch.int16), ref_k.view(torch.int16)), rep
+        assert torch.equal(cache.v_pool.view(torch.int16), ref_v.view(torch.int16)), rep
