@@ -9,6 +9,8 @@ Python binding never import it.
   conditioning set of Sec. 2.1, Eq. 1), optionally with a token-causal
   segment at the end of each block (the thinker's language and state slots,
   Sec. 1 and Sec. 2.4).
+* ``prefill_bwd``: gradients dQ, dK, dV of the whole-sequence path for an
+  upstream output gradient (training uses the same causal format, Sec. 2.3).
 * ``kv_append`` / ``gather`` are the paged full-history cache written out as
   plain per-token loops (the performer appends each received KV slice to its
   own full-history cache, Sec. 2.4).
@@ -52,6 +54,8 @@ def _bind(lib):
     lib.wso_prefill_text.restype = I
     lib.wso_step_text.argtypes = [P, P, P, P, P, I, I, I, I, P, P, I, I, I, D, P, I64, P, P, P, I]
     lib.wso_step_text.restype = I
+    lib.wso_prefill_bwd.argtypes = [P, P, P, P, I, I, I, I, I, I, P, I, P, D, P, P, P, I]
+    lib.wso_prefill_bwd.restype = I
     lib.wso_mutant.restype = I
     return lib
 
@@ -164,6 +168,36 @@ def step(q, k_cache, v_cache, cache_lens, k_new, v_new, scale, rows=None,
     if rc != 0:
         raise ValueError(f"oracle step rejected its arguments (rc={rc})")
     return (out, lse, probs) if want_probs else (out, lse)
+
+
+def prefill_bwd(q, k, v, dout, offsets, scale, text_starts=None, nthreads=None, lib=None):
+    """Gradients of ``prefill`` for an upstream output gradient dout
+    [B][L][Hq][d] (training uses the same causal format, Sec. 2.3).
+    Returns (dq [B][L][Hq][d], dk [B][L][Hkv][d], dv [B][L][Hkv][d]) in
+    float64."""
+    lib = lib or load()
+    q, dt = _as_input(q)
+    k, dtk = _as_input(k)
+    v, dtv = _as_input(v)
+    do, dto = _as_input(dout)
+    assert dt == dtk == dtv == dto
+    B, L, Hq, d = q.shape
+    Hkv = k.shape[2]
+    assert k.shape == (B, L, Hkv, d) and v.shape == k.shape and do.shape == q.shape
+    offsets = np.ascontiguousarray(np.asarray(offsets, dtype=np.int32).reshape(B, -1))
+    nb = offsets.shape[1] - 1
+    ts = None
+    if text_starts is not None:
+        ts = np.ascontiguousarray(np.asarray(text_starts, dtype=np.int32).reshape(B, nb))
+    dq = np.empty((B, L, Hq, d), np.float64)
+    dk = np.empty((B, L, Hkv, d), np.float64)
+    dv = np.empty((B, L, Hkv, d), np.float64)
+    rc = lib.wso_prefill_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(do), dt, B, L, Hq, Hkv, d,
+                             _ptr(offsets), nb, _ptr(ts), float(scale), _ptr(dq), _ptr(dk), _ptr(dv),
+                             int(nthreads or default_threads()))
+    if rc != 0:
+        raise ValueError(f"oracle prefill_bwd rejected its arguments (rc={rc})")
+    return dq, dk, dv
 
 
 def kv_append(k_pool, v_pool, page_table, cache_lens, k_new, v_new):

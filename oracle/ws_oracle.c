@@ -37,6 +37,18 @@
  *
  * Rows are independent, so results do not depend on the thread count.
  *
+ * Gradients (wso_prefill_bwd; training uses the same causal format as
+ * inference, Sec. 2.3): for an upstream gradient dO of the output, with
+ * P_ij the softmax weights above (0 for masked keys),
+ *
+ *   dP_ij = <dO_i, v_j>,   D_i = sum_j P_ij dP_ij,
+ *   dS_ij = P_ij (dP_ij - D_i),
+ *   dQ_i  = scale sum_j dS_ij k_j,
+ *   dK_j  = scale sum_i dS_ij q_i,   dV_j = sum_i P_ij dO_i,
+ *
+ * where the sums over i run over every query row (and, with grouped-query
+ * attention, every query head) that reads KV head g.
+ *
  * Compile-time switch WSO_MUTANT (default 0) plants one deliberate mistake;
  * it exists only so the test suite can show that its pins catch such
  * mistakes.  A normal build never defines it.
@@ -136,30 +148,13 @@ static double wso_key(const wso_job *J, int is_v, int b, int64_t j, int g, int c
     return wso_load(is_v ? &J->v : &J->k, b, j - lc, g, c);
 }
 
-/* Scratch owned by one worker thread. */
-typedef struct {
-    double *s;
-    unsigned char *mask;
-    double *acc;
-} wso_scratch;
-
-/* One query row: materialise the mask row, then the softmax-weighted sum. */
-static void wso_row(const wso_job *J, wso_scratch *S, int b, int h, int64_t i,
-                    double *o, double *lse_out, double *p_out)
+/* Mask row of query i of stream b: mask[j] = 1 iff key j is visible, from
+ * block ids (and the token-causal segment of the query's block).  Positions
+ * are in key order: the query sits at key position iq, its block's segment
+ * starts at key position tau (-1: the block has none). */
+static void wso_mask_row(const wso_job *J, int b, int64_t i, unsigned char *mask)
 {
-    const int G = J->Hq / J->Hkv;
-#if WSO_MUTANT == 3
-    const int g = h % J->Hkv;
-#else
-    const int g = h / G;
-#endif
     const int64_t Lk = wso_num_keys(J, b);
-    const int d = J->d;
-
-    /* 1. explicit mask row from block ids (and the token-causal segment of
-     * the query's block).  Positions are in key order: the query sits at
-     * key position iq, its block's segment starts at key position tau (-1:
-     * the block has none). */
     int beta_q;
     int64_t iq, tau = -1;
     if (J->kind == WSO_PREFILL) {
@@ -197,8 +192,32 @@ static void wso_row(const wso_job *J, wso_scratch *S, int b, int h, int64_t i,
             vis = j < tau || j <= iq;
 #endif
         }
-        S->mask[j] = (unsigned char)vis;
+        mask[j] = (unsigned char)vis;
     }
+}
+
+/* Scratch owned by one worker thread. */
+typedef struct {
+    double *s;
+    unsigned char *mask;
+    double *acc;
+} wso_scratch;
+
+/* One query row: materialise the mask row, then the softmax-weighted sum. */
+static void wso_row(const wso_job *J, wso_scratch *S, int b, int h, int64_t i,
+                    double *o, double *lse_out, double *p_out)
+{
+    const int G = J->Hq / J->Hkv;
+#if WSO_MUTANT == 3
+    const int g = h % J->Hkv;
+#else
+    const int g = h / G;
+#endif
+    const int64_t Lk = wso_num_keys(J, b);
+    const int d = J->d;
+
+    /* 1. explicit mask row */
+    wso_mask_row(J, b, i, S->mask);
 
     /* 2. logits of visible keys, and their maximum */
     double m = -INFINITY;
@@ -495,6 +514,190 @@ int wso_step(const void *q, const void *kc, const void *vc,
 {
     return wso_step_text(q, kc, vc, kn, vn, dtype, B, Lq, Lc_max, cache_lens, NULL, Hq, Hkv, d,
                          scale, rows, nrows, out, lse, probs, nthreads);
+}
+
+/* ---------------------------------------------------------------------- */
+/* Gradients of the whole-sequence path.                                   */
+
+typedef struct {
+    const wso_job *J;
+    const void *dout;
+    double *dq, *dk, *dv;
+    int first, last; /* half-open range of (b, g) groups */
+    int status;
+} wso_bwd_task;
+
+static void *wso_bwd_worker(void *arg)
+{
+    wso_bwd_task *T = (wso_bwd_task *)arg;
+    const wso_job *J = T->J;
+    const int d = J->d, G = J->Hq / J->Hkv;
+    const int64_t L = J->Lq;
+    const wso_view dov = {T->dout, J->q.dtype, J->q.sb, J->q.st, J->q.sh};
+    double *p = (double *)malloc(sizeof(double) * (size_t)(L > 0 ? L : 1));
+    double *dp = (double *)malloc(sizeof(double) * (size_t)(L > 0 ? L : 1));
+    unsigned char *mask = (unsigned char *)malloc((size_t)(L > 0 ? L : 1));
+    if (!p || !dp || !mask) {
+        free(p);
+        free(dp);
+        free(mask);
+        T->status = -1;
+        return NULL;
+    }
+    for (int grp = T->first; grp < T->last; ++grp) {
+        const int b = grp / J->Hkv, g = grp % J->Hkv;
+        for (int hh = 0; hh < G; ++hh) {
+            const int h = g * G + hh;
+            for (int64_t i = 0; i < L; ++i) {
+                /* softmax weights of row i over its visible keys */
+                wso_mask_row(J, b, i, mask);
+                double m = -INFINITY;
+                for (int64_t j = 0; j < L; ++j) {
+                    if (!mask[j])
+                        continue;
+                    double dot = 0.0;
+                    for (int c = 0; c < d; ++c)
+                        dot += wso_load(&J->q, b, i, h, c) * wso_load(&J->k, b, j, g, c);
+                    p[j] = J->scale * dot;
+                    if (p[j] > m)
+                        m = p[j];
+                }
+                double l = 0.0;
+                for (int64_t j = 0; j < L; ++j) {
+                    p[j] = mask[j] ? exp(p[j] - m) : 0.0;
+                    l += p[j];
+                }
+                for (int64_t j = 0; j < L; ++j)
+                    p[j] /= l;
+                /* dP_ij = <dO_i, v_j>, D_i = sum_j P_ij dP_ij */
+                double D = 0.0;
+                for (int64_t j = 0; j < L; ++j) {
+                    dp[j] = 0.0;
+                    if (!mask[j])
+                        continue;
+                    for (int c = 0; c < d; ++c)
+                        dp[j] += wso_load(&dov, b, i, h, c) * wso_load(&J->v, b, j, g, c);
+                    D += p[j] * dp[j];
+                }
+                /* dS_ij = P_ij (dP_ij - D_i) and the three gradients */
+                double *dqi = T->dq + (((int64_t)b * L + i) * J->Hq + h) * d;
+                for (int c = 0; c < d; ++c)
+                    dqi[c] = 0.0;
+                for (int64_t j = 0; j < L; ++j) {
+                    if (!mask[j])
+                        continue;
+#if WSO_MUTANT == 11
+                    const double ds = p[j] * dp[j];
+#else
+                    const double ds = p[j] * (dp[j] - D);
+#endif
+                    double *dkj = T->dk + (((int64_t)b * L + j) * J->Hkv + g) * d;
+                    double *dvj = T->dv + (((int64_t)b * L + j) * J->Hkv + g) * d;
+                    for (int c = 0; c < d; ++c) {
+                        dqi[c] += J->scale * ds * wso_load(&J->k, b, j, g, c);
+#if WSO_MUTANT == 12
+                        dkj[c] += ds * wso_load(&J->q, b, i, h, c);
+#else
+                        dkj[c] += J->scale * ds * wso_load(&J->q, b, i, h, c);
+#endif
+                        dvj[c] += p[j] * wso_load(&dov, b, i, h, c);
+                    }
+                }
+            }
+        }
+    }
+    free(p);
+    free(dp);
+    free(mask);
+    T->status = 0;
+    return NULL;
+}
+
+/*
+ * Gradients of whole-sequence block-causal attention (with optional
+ * token-causal segments, as wso_prefill_text).  q, dout: [B][L][Hq][d];
+ * k, v: [B][L][Hkv][d]; all contiguous, dtype WSO_F64 or WSO_BF16.
+ * Outputs (fp64, overwritten): dq [B][L][Hq][d], dk and dv [B][L][Hkv][d].
+ * Threads split the (stream, KV head) groups, so every gradient sum runs
+ * in a fixed order whatever the thread count.
+ * Returns 0 on success, -2 on bad arguments, -1 on allocation failure.
+ */
+int wso_prefill_bwd(const void *q, const void *k, const void *v, const void *dout, int dtype,
+                    int B, int L, int Hq, int Hkv, int d,
+                    const int32_t *offsets, int nb, const int32_t *text_starts, double scale,
+                    double *dq, double *dk, double *dv, int nthreads)
+{
+    if (wso_check_common(B, L, Hq, Hkv, d) || nb < 0 || !offsets || !dq || !dk || !dv || !dout)
+        return -2;
+    for (int b = 0; b < B; ++b) {
+        const int32_t *off = offsets + (int64_t)b * (nb + 1);
+        if (off[0] != 0 || off[nb] != L)
+            return -2;
+        for (int n = 0; n < nb; ++n) {
+            if (off[n + 1] < off[n])
+                return -2;
+            if (text_starts) {
+                const int32_t t = text_starts[(int64_t)b * nb + n];
+                if (t < off[n] || t > off[n + 1])
+                    return -2;
+            }
+        }
+    }
+    wso_job J;
+    memset(&J, 0, sizeof J);
+    J.kind = WSO_PREFILL;
+    J.B = B; J.Lq = L; J.Hq = Hq; J.Hkv = Hkv; J.d = d;
+    J.scale = scale;
+    J.q = (wso_view){q, dtype, (int64_t)L * Hq * d, (int64_t)Hq * d, d};
+    J.k = (wso_view){k, dtype, (int64_t)L * Hkv * d, (int64_t)Hkv * d, d};
+    J.v = (wso_view){v, dtype, (int64_t)L * Hkv * d, (int64_t)Hkv * d, d};
+    J.offsets = offsets;
+    J.nb = nb;
+    J.text_starts = text_starts;
+    const int64_t nkv = (int64_t)B * L * Hkv * d;
+    for (int64_t x = 0; x < nkv; ++x) {
+        dk[x] = 0.0;
+        dv[x] = 0.0;
+    }
+    const int groups = B * Hkv;
+    if (groups == 0 || L == 0)
+        return 0;
+    if (nthreads < 1)
+        nthreads = 1;
+    if (nthreads > groups)
+        nthreads = groups;
+    pthread_t *th = (pthread_t *)calloc((size_t)nthreads, sizeof(pthread_t));
+    wso_bwd_task *tasks = (wso_bwd_task *)calloc((size_t)nthreads, sizeof(wso_bwd_task));
+    if (!th || !tasks) {
+        free(th);
+        free(tasks);
+        return -1;
+    }
+    for (int t = 0; t < nthreads; ++t) {
+        tasks[t] = (wso_bwd_task){&J, dout, dq, dk, dv, groups * t / nthreads,
+                                  groups * (t + 1) / nthreads, -1};
+    }
+    int started = 0;
+    for (int t = 1; t < nthreads; ++t) {
+        if (pthread_create(&th[t], NULL, wso_bwd_worker, &tasks[t]) != 0)
+            break;
+        started = t;
+    }
+    wso_bwd_worker(&tasks[0]);
+    int rc = tasks[0].status;
+    for (int t = 1; t <= started; ++t) {
+        pthread_join(th[t], NULL);
+        if (tasks[t].status != 0)
+            rc = -1;
+    }
+    for (int t = started + 1; t < nthreads; ++t) {
+        wso_bwd_worker(&tasks[t]);
+        if (tasks[t].status != 0)
+            rc = -1;
+    }
+    free(th);
+    free(tasks);
+    return rc;
 }
 
 int wso_mutant(void) { return WSO_MUTANT; }

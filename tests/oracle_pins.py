@@ -11,7 +11,8 @@ The rule being pinned (Wan-Streamer v0.1, Abstract, Sec. 1 with Fig. 1 and
 Sec. 5: block-causal attention over the interleaved stream; Sec. 2.1, Eq. 1:
 unit k is conditioned on inputs of units <= k and responses of units < k):
 a token sees every token of its own block and of every earlier block, and
-nothing later.  With a token-causal segment at the end of a block (the
+nothing later (and, for the gradients, the chain rule through that
+softmax).  With a token-causal segment at the end of a block (the
 thinker's language and state slots, decoded token by token: Sec. 1 and
 Sec. 2.4; next-token prediction of language, Sec. 2.1), the block's
 observation tokens (before the segment) see each other but not the segment,
@@ -423,6 +424,110 @@ def pin_streaming_equals_prefill_text(lib):
         assert np.array_equal(sl, lse[:, :, s:e]), j
 
 
+# --------------------------------------------------------------------------
+# gradients (training uses the same causal format, Sec. 2.3)
+
+def _visible(ids, starts, L):
+    """Boolean [L][L] visibility from block ids and segment starts, written
+    from the rule: earlier blocks, and inside the block observations (before
+    the segment start) plus segment tokens up to the query."""
+    vis = np.zeros((L, L), bool)
+    for i in range(L):
+        for j in range(L):
+            same = ids[j] == ids[i]
+            vis[i, j] = ids[j] < ids[i] or (same and (j < starts[ids[i]] or j <= i))
+    return vis
+
+
+def pin_bwd_matches_autograd(lib):
+    """fp64 autograd through torch's scaled_dot_product_attention with the
+    boolean mask of random block/segment layouts (GQA by repeating K/V)."""
+    rng = _rng(41)
+    for trial in range(4):
+        B, L, Hkv, G, d = 1, 23, 2, 2, 6
+        Hq = Hkv * G
+        offs = _random_offsets(rng, L, 5)
+        starts = np.array([rng.integers(offs[n], offs[n + 1] + 1) for n in range(5)], np.int32)
+        text = None if trial == 0 else starts[None]
+        q, do = (rng.standard_normal((B, L, Hq, d)) for _ in range(2))
+        k, v = (rng.standard_normal((B, L, Hkv, d)) for _ in range(2))
+        scale = 0.45
+        dq, dk, dv = oracle.prefill_bwd(q, k, v, do, offs[None], scale, text_starts=text, lib=lib)
+        ids = [int(np.searchsorted(offs, t, side="right") - 1) for t in range(L)]
+        ids = [min(x, 4) for x in ids]
+        vis = _visible(ids, starts if text is not None else offs[1:], L)
+        tq, tk, tv = (torch.from_numpy(a.copy()).requires_grad_(True) for a in (q, k, v))
+        kk = tk.repeat_interleave(G, dim=2).permute(0, 2, 1, 3)
+        vv = tv.repeat_interleave(G, dim=2).permute(0, 2, 1, 3)
+        o = torch.nn.functional.scaled_dot_product_attention(
+            tq.permute(0, 2, 1, 3), kk, vv, attn_mask=torch.from_numpy(vis), scale=scale)
+        o.permute(0, 2, 1, 3).backward(torch.from_numpy(do))
+        assert np.max(np.abs(dq - tq.grad.numpy())) <= 1e-11, trial
+        assert np.max(np.abs(dk - tk.grad.numpy())) <= 1e-11, trial
+        assert np.max(np.abs(dv - tv.grad.numpy())) <= 1e-11, trial
+
+
+def pin_bwd_finite_differences(lib):
+    """Central differences of the oracle's own forward: d<O, dO>/dx."""
+    rng = _rng(42)
+    B, L, Hq, Hkv, d = 1, 7, 2, 1, 3
+    q, do = (rng.standard_normal((B, L, Hq, d)) for _ in range(2))
+    k, v = (rng.standard_normal((B, L, Hkv, d)) for _ in range(2))
+    offs = np.array([[0, 2, 3, 7]], np.int32)
+    starts = np.array([[1, 3, 5]], np.int32)
+    scale = 0.7
+    grads = oracle.prefill_bwd(q, k, v, do, offs, scale, text_starts=starts, lib=lib)
+
+    def loss(q_, k_, v_):
+        o, _ = oracle.prefill(q_, k_, v_, offs, scale, lib=lib, text_starts=starts)
+        return float(np.sum(o * do))
+
+    h = 1e-6
+    for which, (x, g) in enumerate(zip((q, k, v), grads)):
+        for idx in np.ndindex(*x.shape):
+            xp, xm = x.copy(), x.copy()
+            xp[idx] += h
+            xm[idx] -= h
+            args_p = [q, k, v]
+            args_m = [q, k, v]
+            args_p[which], args_m[which] = xp, xm
+            fd = (loss(*args_p) - loss(*args_m)) / (2 * h)
+            assert abs(fd - g[idx]) <= 1e-7, (which, idx, fd, g[idx])
+
+
+def pin_bwd_closed_forms(lib):
+    """Rows of P sum to 1, so the dV of all keys sums to the sum of dO over
+    the group's query rows and heads; rows of dS sum to 0, so the dK of all
+    keys sums to 0; constant values make dS = 0, so dQ = dK = 0."""
+    rng = _rng(43)
+    B, L, Hkv, G, d = 2, 19, 2, 3, 4
+    Hq = Hkv * G
+    q, do = (rng.standard_normal((B, L, Hq, d)) for _ in range(2))
+    k, v = (rng.standard_normal((B, L, Hkv, d)) for _ in range(2))
+    offs = np.stack([_random_offsets(rng, L, 4) for _ in range(B)])
+    dq, dk, dv = oracle.prefill_bwd(q, k, v, do, offs, 0.6, lib=lib)
+    for g in range(Hkv):
+        sum_do = do[:, :, g * G:(g + 1) * G].sum(axis=(1, 2))
+        assert np.max(np.abs(dv[:, :, g].sum(axis=1) - sum_do)) <= 1e-12
+    assert np.max(np.abs(dk.sum(axis=1))) <= 1e-12
+    c = rng.standard_normal(d)
+    vc = np.broadcast_to(c, v.shape).copy()
+    dq, dk, dv = oracle.prefill_bwd(q, k, vc, do, offs, 0.6, lib=lib)
+    assert np.max(np.abs(dq)) <= 1e-13 and np.max(np.abs(dk)) <= 1e-13
+
+
+def pin_bwd_later_block_keeps_earlier_dq(lib):
+    """A later block (invisible to earlier rows) leaves the earlier rows'
+    dQ bitwise unchanged."""
+    rng = _rng(44)
+    B, L, H, d, extra = 1, 20, 2, 5, 6
+    q, k, v, do = (rng.standard_normal((B, L + extra, H, d)) for _ in range(4))
+    base = _random_offsets(rng, L, 3)
+    dq1, _, _ = oracle.prefill_bwd(q[:, :L], k[:, :L], v[:, :L], do[:, :L], base[None], 0.5, lib=lib)
+    dq2, _, _ = oracle.prefill_bwd(q, k, v, do, np.append(base, L + extra)[None].astype(np.int32), 0.5, lib=lib)
+    assert np.array_equal(dq1, dq2[:, :L])
+
+
 ALL_PINS = [
     pin_bruteforce_all_compositions,
     pin_single_block_is_full_attention,
@@ -443,6 +548,10 @@ ALL_PINS = [
     pin_empty_segments_are_block_causal,
     pin_zero_query_text_counts,
     pin_streaming_equals_prefill_text,
+    pin_bwd_matches_autograd,
+    pin_bwd_finite_differences,
+    pin_bwd_closed_forms,
+    pin_bwd_later_block_keeps_earlier_dq,
 ]
 
 # the deliberately broken oracle builds (see WSO_MUTANT in ws_oracle.c)
@@ -457,4 +566,6 @@ MUTANTS = {
     8: "mask direction reversed",
     9: "segment token sees the next segment token",
     10: "observation tokens see their block's segment",
+    11: "gradient: D_i term dropped from dS",
+    12: "gradient: scale dropped from dK",
 }
