@@ -99,7 +99,7 @@ enum { WS_DTYPE_BF16 = 1, WS_DTYPE_F32 = 2 };
 enum { WS_FUSE_APPEND = 1 };
 
 /* op codes of ws_workspace_bytes */
-enum { WS_OP_STEP = 1, WS_OP_PREFILL = 2 };
+enum { WS_OP_STEP = 1, WS_OP_PREFILL = 2, WS_OP_PREFILL_BWD = 3 };
 
 /* A [batch][tokens][heads][head_dim] tensor; head_dim contiguous; strides in elements. */
 typedef struct {
@@ -263,11 +263,48 @@ int ws_block_causal_prefill_text(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v,
                                  float scale, ws_tensor4 out, float *lse, void *stream);
 
 /*
+ * ws_block_causal_prefill_bwd -- gradients of ws_block_causal_prefill(_text)
+ * for training (Sec. 2.3: training uses the same causal format as
+ * inference).  For an upstream gradient dO of the output, with P the
+ * softmax weights of the forward (0 for masked keys):
+ *   D_i = <dO_i, O_i>,  dS_ij = P_ij (<dO_i, v_j> - D_i),
+ *   dQ_i = scale sum_j dS_ij k_j,  dK_j = scale sum_i dS_ij q_i,
+ *   dV_j = sum_i P_ij dO_i,
+ * the sums over i running over every query row and query head that reads
+ * KV head floor(h / G).
+ *   q, o, dout: bf16 [batch][seq_len][num_q_heads][head_dim]; o is the
+ *               forward's output (its bf16 values enter D)
+ *   k, v:       bf16 [batch][seq_len][num_kv_heads][head_dim] (contiguous
+ *               keys; no paged variant)
+ *   lse:        device f32 [batch][num_q_heads][seq_len], the forward's lse
+ *   block_offsets_host / _dev: as ws_block_causal_prefill
+ *   text_starts_host / _dev:   NULL / NULL for block-causal, or as
+ *               ws_block_causal_prefill_text
+ *   dq:         f32 [batch][seq_len][num_q_heads][head_dim] (written)
+ *   dk, dv:     f32 [batch][seq_len][num_kv_heads][head_dim] (written)
+ *   workspace:  device scratch of ws_workspace_bytes(WS_OP_PREFILL_BWD,
+ *               batch, num_q_heads, num_kv_heads, seq_len, seq_len) bytes,
+ *               16-byte aligned; contents on entry ignored
+ * The gradients are deterministic (fixed summation order; no atomics).
+ * Errors: WS_ERR_NULL, WS_ERR_SHAPE, WS_ERR_UNSUPPORTED, WS_ERR_ALIGN,
+ * WS_ERR_HEADS, WS_ERR_OFFSETS, WS_ERR_WORKSPACE, WS_ERR_HIP.
+ */
+int ws_block_causal_prefill_bwd(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, ws_tensor4 o,
+                                ws_tensor4 dout, const float *lse,
+                                const int32_t *block_offsets_host, const int32_t *block_offsets_dev,
+                                const int32_t *text_starts_host, const int32_t *text_starts_dev,
+                                int32_t batch, int32_t seq_len, int32_t num_blocks,
+                                int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                float scale, ws_tensor4 dq, ws_tensor4 dk, ws_tensor4 dv,
+                                void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * Workspace bytes ws_block_causal_attn_fwd (and its _text variant) needs
  * for this shape (op =
  * WS_OP_STEP; num_kv_heads = the cache's; max_k = largest cache_lens[b] +
- * new_len).  WS_OP_PREFILL returns 0.  Pure host arithmetic; returns 0 for
- * invalid arguments.
+ * new_len).  WS_OP_PREFILL returns 0.  WS_OP_PREFILL_BWD (max_q = max_k =
+ * seq_len): the bytes ws_block_causal_prefill_bwd needs.  Pure host
+ * arithmetic; returns 0 for invalid arguments.
  */
 size_t ws_workspace_bytes(int32_t op, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
                           int32_t max_q, int32_t max_k);

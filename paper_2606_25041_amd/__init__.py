@@ -11,6 +11,7 @@ Entry points (same names as the C ABI, without the ``ws_`` prefix):
   block_causal_prefill(q, k, v, block_offsets, ..., text_starts=None)
 (with text_starts: the *_text entry points, blocks ending in a token-causal
 segment)
+  block_causal_prefill_bwd(q, k, v, o, dout, lse, block_offsets, ...)
   workspace_bytes(op, batch, num_q_heads, num_kv_heads, max_q, max_k)
 """
 import ctypes
@@ -22,12 +23,12 @@ import torch  # loads the HIP runtime that libwsattn.so then shares
 from . import build as _build
 
 __all__ = ["WsError", "PagedCache", "kv_append", "block_causal_attn_fwd",
-           "block_causal_prefill", "workspace_bytes", "library", "abi_version",
-           "WS_OP_STEP", "WS_OP_PREFILL", "PAGE_SIZE"]
+           "block_causal_prefill", "block_causal_prefill_bwd", "workspace_bytes", "library",
+           "abi_version", "WS_OP_STEP", "WS_OP_PREFILL", "WS_OP_PREFILL_BWD", "PAGE_SIZE"]
 
 WS_DTYPE_BF16, WS_DTYPE_F32 = 1, 2
 WS_FUSE_APPEND = 1
-WS_OP_STEP, WS_OP_PREFILL = 1, 2
+WS_OP_STEP, WS_OP_PREFILL, WS_OP_PREFILL_BWD = 1, 2, 3
 PAGE_SIZE = 64
 STATUS = {0: "WS_OK", 1: "WS_ERR_NULL", 2: "WS_ERR_SHAPE", 3: "WS_ERR_UNSUPPORTED",
           4: "WS_ERR_ALIGN", 5: "WS_ERR_OFFSETS", 6: "WS_ERR_PAGE", 7: "WS_ERR_CAPACITY",
@@ -90,6 +91,10 @@ def library():
         lib.ws_block_causal_prefill_text.argtypes = [
             Tensor4, Tensor4, Tensor4, ctypes.POINTER(PagedKVDesc), P, P, P, P, I32, I32, I32, I32, I32,
             I32, F, Tensor4, P, P]
+        lib.ws_block_causal_prefill_bwd.restype = ctypes.c_int
+        lib.ws_block_causal_prefill_bwd.argtypes = [
+            Tensor4, Tensor4, Tensor4, Tensor4, Tensor4, P, P, P, P, P, I32, I32, I32, I32, I32, I32, F,
+            Tensor4, Tensor4, Tensor4, P, ctypes.c_size_t, P]
         if lib.ws_abi_version() != 3:
             raise RuntimeError("libwsattn.so ABI version mismatch")
         _LIB = lib
@@ -315,3 +320,46 @@ def block_causal_prefill(q, k, v, block_offsets, scale=None, cache=None, num_kv_
             _t4(q), _t4(k), _t4(v), kvp, off_h.data_ptr(), off_d.data_ptr(), th.data_ptr(), td.data_ptr(),
             B, L, nb, Hq, hkv, D, float(scale), _t4(out), _ptr(lse), _stream()))
     return (out, lse) if want_lse else out
+
+
+def block_causal_prefill_bwd(q, k, v, o, dout, lse, block_offsets, scale=None, text_starts=None,
+                             dq=None, dk=None, dv=None, workspace=None):
+    """Gradients of ``block_causal_prefill`` (contiguous K/V) for an upstream
+    output gradient dout: returns f32 (dq [B][L][Hq][d], dk, dv
+    [B][L][Hkv][d]).  o and lse are the forward's output and lse;
+    text_starts as in ``block_causal_prefill``."""
+    B, L, Hq, D = q.shape
+    hkv = k.shape[2]
+    if isinstance(block_offsets, tuple):
+        off_h, off_d = block_offsets
+    else:
+        off_h = torch.as_tensor(block_offsets, dtype=torch.int32).cpu().contiguous()
+        off_d = off_h.to(q.device)
+    nb = off_h.shape[-1] - 1
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    for name, t, shp in (("k", k, (B, L, hkv, D)), ("v", v, (B, L, hkv, D)), ("o", o, (B, L, Hq, D)),
+                         ("dout", dout, (B, L, Hq, D)), ("lse", lse, (B, Hq, L))):
+        _shape(name, t, shp)
+    if tuple(off_h.shape) != (B, nb + 1) or tuple(off_d.shape) != (B, nb + 1):
+        raise ValueError("block_offsets must be [B][num_blocks + 1]")
+    if dq is None:
+        dq = torch.empty((B, L, Hq, D), dtype=torch.float32, device=q.device)
+    if dk is None:
+        dk = torch.empty((B, L, hkv, D), dtype=torch.float32, device=q.device)
+    if dv is None:
+        dv = torch.empty((B, L, hkv, D), dtype=torch.float32, device=q.device)
+    _shape("dq", dq, (B, L, Hq, D))
+    _shape("dk", dk, (B, L, hkv, D))
+    _shape("dv", dv, (B, L, hkv, D))
+    need = workspace_bytes(WS_OP_PREFILL_BWD, B, Hq, hkv, L, L) if B > 0 and L > 0 else 0
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    th = td = None
+    if text_starts is not None:
+        th, td = _int32_pair(text_starts, (B, nb), q.device)
+    _check(library().ws_block_causal_prefill_bwd(
+        _t4(q), _t4(k), _t4(v), _t4(o), _t4(dout), _ptr(lse), off_h.data_ptr(), off_d.data_ptr(),
+        _ptr(th), _ptr(td), B, L, nb, Hq, hkv, D, float(scale), _t4(dq), _t4(dk), _t4(dv),
+        _ptr(workspace), workspace.numel() if workspace is not None else 0, _stream()))
+    return dq, dk, dv

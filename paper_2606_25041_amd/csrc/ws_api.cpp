@@ -147,6 +147,15 @@ size_t step_workspace(const StepPlan &p, int batch, int hq, int hkv, int lq) {
 
 ws::TileShape plan_prefill(int) { return default_shape(); }
 
+// Backward workspace: (lse * log2 e, <dO, O>) per row as f32 pairs, then the
+// key end of each token (int32), at a 256-byte aligned offset.
+size_t bwd_dl_bytes(int batch, int hq, int seq) {
+    return ((size_t)batch * hq * seq * 2 * sizeof(float) + 255) / 256 * 256;
+}
+size_t bwd_workspace(int batch, int hq, int seq) {
+    return bwd_dl_bytes(batch, hq, seq) + (size_t)batch * seq * sizeof(int32_t);
+}
+
 // Total work items; fails when the grid would not fit the kernel's int math.
 bool finish_work(ws::AttnArgs &a) {
     const int64_t n = (int64_t)a.B * a.Hkv * a.gi * a.nqt * a.nsplit;
@@ -204,6 +213,11 @@ const char *ws_last_error(void) { return g_err; }
 
 size_t ws_workspace_bytes(int32_t op, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
                           int32_t max_q, int32_t max_k) {
+    if (op == WS_OP_PREFILL_BWD) {
+        if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads || max_q <= 0)
+            return 0;
+        return bwd_workspace(batch, num_q_heads, max_q);
+    }
     if (op != WS_OP_STEP) return 0;
     if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads || max_q <= 0 ||
         max_k < max_q)
@@ -280,6 +294,82 @@ int ws_block_causal_prefill_text(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, const
     return prefill_impl(q, k, v, kv_or_null, block_offsets_host, block_offsets_dev, text_starts_host,
                         text_starts_dev, batch, seq_len, num_blocks, num_q_heads, num_kv_heads, head_dim,
                         scale, out, lse, stream);
+}
+
+int ws_block_causal_prefill_bwd(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, ws_tensor4 o, ws_tensor4 dout,
+                                const float *lse, const int32_t *block_offsets_host,
+                                const int32_t *block_offsets_dev, const int32_t *text_starts_host,
+                                const int32_t *text_starts_dev, int32_t batch, int32_t seq_len, int32_t num_blocks,
+                                int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, float scale,
+                                ws_tensor4 dq, ws_tensor4 dk, ws_tensor4 dv, void *workspace,
+                                size_t workspace_bytes, void *stream) {
+    if (batch < 0 || seq_len < 0 || num_blocks < 0 || num_q_heads <= 0 || num_kv_heads <= 0)
+        return fail(WS_ERR_SHAPE, "batch %d, seq_len %d, num_blocks %d, heads %d/%d", (int)batch, (int)seq_len,
+                    (int)num_blocks, (int)num_q_heads, (int)num_kv_heads);
+    if (batch == 0 || seq_len == 0) return ok();
+    if (int rc = check_tensor("q", q, false)) return rc;
+    if (int rc = check_tensor("k", k, false)) return rc;
+    if (int rc = check_tensor("v", v, false)) return rc;
+    if (int rc = check_tensor("o", o, false)) return rc;
+    if (int rc = check_tensor("dout", dout, false)) return rc;
+    if (int rc = check_tensor("dq", dq, true)) return rc;
+    if (int rc = check_tensor("dk", dk, true)) return rc;
+    if (int rc = check_tensor("dv", dv, true)) return rc;
+    if (dq.dtype != WS_DTYPE_F32 || dk.dtype != WS_DTYPE_F32 || dv.dtype != WS_DTYPE_F32)
+        return fail(WS_ERR_UNSUPPORTED, "dq, dk and dv must be f32");
+    if (!lse) return fail(WS_ERR_NULL, "lse is NULL");
+    if ((uintptr_t)lse & 3u) return fail(WS_ERR_ALIGN, "lse must be 4-byte aligned");
+    if (!block_offsets_host || !block_offsets_dev) return fail(WS_ERR_NULL, "block offsets pointer is NULL");
+    if (!text_starts_host != !text_starts_dev) return fail(WS_ERR_NULL, "text_starts: give both copies or neither");
+    if (int rc = check_head_dim(head_dim)) return rc;
+    if (!(scale > 0.f) || !std::isfinite(scale)) return fail(WS_ERR_UNSUPPORTED, "scale must be finite and > 0");
+    if (num_q_heads % num_kv_heads)
+        return fail(WS_ERR_HEADS, "num_q_heads %d not a multiple of num_kv_heads %d", (int)num_q_heads,
+                    (int)num_kv_heads);
+    for (int b = 0; b < batch; ++b) {
+        const int32_t *off = block_offsets_host + (int64_t)b * (num_blocks + 1);
+        if (off[0] != 0) return fail(WS_ERR_OFFSETS, "block_offsets[%d][0] = %d, must be 0", b, (int)off[0]);
+        for (int n = 0; n < num_blocks; ++n) {
+            if (off[n + 1] < off[n])
+                return fail(WS_ERR_OFFSETS, "block_offsets[%d] decreases at %d", b, n + 1);
+            if (text_starts_host) {
+                const int32_t t = text_starts_host[(int64_t)b * num_blocks + n];
+                if (t < off[n] || t > off[n + 1])
+                    return fail(WS_ERR_OFFSETS, "text_starts[%d][%d] = %d outside block [%d, %d]", b, n, (int)t,
+                                (int)off[n], (int)off[n + 1]);
+            }
+        }
+        if (off[num_blocks] != seq_len)
+            return fail(WS_ERR_OFFSETS, "block_offsets[%d][%d] = %d, must equal seq_len %d", b, (int)num_blocks,
+                        (int)off[num_blocks], (int)seq_len);
+    }
+    const int64_t work = (int64_t)batch * num_q_heads * ((seq_len + 127) / 128);
+    if (work > INT32_MAX) return fail(WS_ERR_SHAPE, "too many work items");
+    const size_t need = bwd_workspace(batch, num_q_heads, seq_len);
+    if (!workspace || workspace_bytes < need || !aligned16(workspace))
+        return fail(WS_ERR_WORKSPACE, "workspace needs %zu bytes (16-byte aligned), got %zu", need,
+                    workspace ? workspace_bytes : (size_t)0);
+    ws::BwdArgs a{};
+    a.q = (const uint16_t *)q.ptr; a.q_sb = q.stride_b; a.q_st = q.stride_t; a.q_sh = q.stride_h;
+    a.k = (const uint16_t *)k.ptr; a.k_sb = k.stride_b; a.k_st = k.stride_t; a.k_sh = k.stride_h;
+    a.v = (const uint16_t *)v.ptr; a.v_sb = v.stride_b; a.v_st = v.stride_t; a.v_sh = v.stride_h;
+    a.o = (const uint16_t *)o.ptr; a.o_sb = o.stride_b; a.o_st = o.stride_t; a.o_sh = o.stride_h;
+    a.dout = (const uint16_t *)dout.ptr; a.do_sb = dout.stride_b; a.do_st = dout.stride_t; a.do_sh = dout.stride_h;
+    a.lse = lse;
+    a.offsets = block_offsets_dev;
+    a.text_starts = text_starts_dev;
+    a.nb = num_blocks;
+    a.dq = (float *)dq.ptr; a.dq_sb = dq.stride_b; a.dq_st = dq.stride_t; a.dq_sh = dq.stride_h;
+    a.dk = (float *)dk.ptr; a.dk_sb = dk.stride_b; a.dk_st = dk.stride_t; a.dk_sh = dk.stride_h;
+    a.dv = (float *)dv.ptr; a.dv_sb = dv.stride_b; a.dv_st = dv.stride_t; a.dv_sh = dv.stride_h;
+    a.dl = (float *)workspace;
+    a.kend = (int32_t *)((char *)workspace + bwd_dl_bytes(batch, num_q_heads, seq_len));
+    a.B = batch; a.L = seq_len; a.Hq = num_q_heads; a.Hkv = num_kv_heads; a.G = num_q_heads / num_kv_heads;
+    a.scale = scale;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    if (int e = ws::launch_prefill_bwd(a, head_dim, stream))
+        return fail(WS_ERR_HIP, "backward launch failed (hip error %d)", e);
+    return ok();
 }
 
 }  // extern "C"

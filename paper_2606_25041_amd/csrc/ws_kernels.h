@@ -109,6 +109,31 @@ struct AppendArgs {
     int32_t B, Ln, Hkv, D;
 };
 
+// Gradients of the whole-sequence path (contiguous K/V).  bf16 inputs,
+// f32 gradients; element strides.
+struct BwdArgs {
+    const uint16_t *q, *k, *v, *o, *dout;
+    int64_t q_sb, q_st, q_sh;
+    int64_t k_sb, k_st, k_sh;
+    int64_t v_sb, v_st, v_sh;
+    int64_t o_sb, o_st, o_sh;
+    int64_t do_sb, do_st, do_sh;
+    const float *lse;            // forward lse [B][Hq][L] (natural log)
+    const int32_t *offsets;      // [B][nb+1]
+    const int32_t *text_starts;  // [B][nb] or nullptr
+    int32_t nb;
+    float *dq, *dk, *dv;
+    int64_t dq_sb, dq_st, dq_sh;
+    int64_t dk_sb, dk_st, dk_sh;
+    int64_t dv_sb, dv_st, dv_sh;
+    // workspace: per row (lse * log2(e), rowsum(dO * O)) [B][Hq][L], and the
+    // end of the keys each token sees [B][L]
+    float *dl;
+    int32_t *kend;
+    int32_t B, L, Hq, Hkv, G;
+    float scale, scale_log2;
+};
+
 // Launch shapes compiled into the library.
 struct TileShape {
     int nb;  // 32-query column blocks per wave
@@ -122,5 +147,7 @@ struct TileShape {
 int launch_attention(const AttnArgs &a, int head_dim, TileShape shape, void *stream);
 int launch_combine(const AttnArgs &a, int head_dim, void *stream);
 int launch_append(const AppendArgs &a, void *stream);
+// prep (row sums, key ends), then dQ and dK/dV; 0 or a HIP error code
+int launch_prefill_bwd(const BwdArgs &a, int head_dim, void *stream);
 
 }  // namespace ws

@@ -41,7 +41,7 @@ def header_functions():
 def test_exports_every_declared_symbol(lib):
     names = header_functions()
     assert {"ws_kv_append", "ws_block_causal_attn_fwd", "ws_block_causal_prefill",
-            "ws_block_causal_attn_fwd_text", "ws_block_causal_prefill_text",
+            "ws_block_causal_attn_fwd_text", "ws_block_causal_prefill_text", "ws_block_causal_prefill_bwd",
             "ws_workspace_bytes", "ws_abi_version", "ws_status_string", "ws_last_error"} <= set(names)
     for name in names:
         assert hasattr(lib, name), name
@@ -224,6 +224,34 @@ def test_prefill_text_errors(lib):
     # starts at the block bounds are valid: the call reaches a later check
     assert prefill_text_call(lib, [[0, 5, 5, 9]], [[5, 5, 5]], lse=FAKE + 2) == 4
     assert prefill_text_call(lib, [[0, 5, 9]], [[0, 9]], lse=FAKE + 2) == 4
+
+
+def bwd_call(lib, offs, B=1, Hq=4, Hkv=2, d=128, lse=FAKE, wsp=FAKE, wsb=1 << 30, dq_dtype=ws.WS_DTYPE_F32,
+             text=None, text_dev=None):
+    offs = np.ascontiguousarray(np.asarray(offs, np.int32))
+    L = int(offs.reshape(B, -1)[0, -1])
+    nb = offs.reshape(B, -1).shape[1] - 1
+    f32 = lambda H: t4(dtype=dq_dtype, H=H, L=L, d=d, sh=d, st=H * d, sb=L * H * d)
+    tx = np.ascontiguousarray(np.asarray(text, np.int32)) if text is not None else None
+    return lib.ws_block_causal_prefill_bwd(t4(H=Hq, L=L, d=d), t4(H=Hkv, L=L, d=d), t4(H=Hkv, L=L, d=d),
+                                           t4(H=Hq, L=L, d=d), t4(H=Hq, L=L, d=d), lse, offs.ctypes.data, FAKE,
+                                           tx.ctypes.data if tx is not None else None, text_dev, B, L, nb, Hq, Hkv,
+                                           d, 0.1, f32(Hq), f32(Hkv), f32(Hkv), wsp, wsb, None)
+
+
+def test_bwd_errors(lib):
+    assert bwd_call(lib, [[0, 5, 9]], lse=None) == 1
+    assert bwd_call(lib, [[0, 5, 9]], text=[[0, 5]]) == 1          # host starts without device copy
+    assert bwd_call(lib, [[0, 5, 9]], dq_dtype=ws.WS_DTYPE_BF16) == 3
+    assert bwd_call(lib, [[0, 5, 9]], d=96) == 3
+    assert bwd_call(lib, [[0, 5, 9]], Hq=3) == 8
+    assert bwd_call(lib, [[1, 5, 9]]) == 5
+    assert bwd_call(lib, [[0, 5, 9]], text=[[6, 7]], text_dev=FAKE) == 5
+    assert bwd_call(lib, [[0, 5, 9]], wsp=None) == 9
+    assert bwd_call(lib, [[0, 5, 9]], wsb=16) == 9
+    assert bwd_call(lib, [[0, 5, 9]], lse=FAKE + 2) == 4
+    n = lib.ws_workspace_bytes(ws.WS_OP_PREFILL_BWD, 2, 32, 8, 16384, 16384)
+    assert n == 2 * 32 * 16384 * 8 + 2 * 16384 * 4
 
 
 def test_empty_calls_are_ok(lib):

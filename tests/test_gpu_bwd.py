@@ -1,0 +1,91 @@
+"""GPU parity of the gradients (training uses the same causal format,
+Sec. 2.3): ws_block_causal_prefill_bwd, fed with the GPU forward's output
+and lse, against the fp64 oracle's dQ, dK, dV on the same bf16 inputs and
+upstream gradient.  Tolerance: max-abs 2e-2 and mean-abs 2e-3 (the
+output tolerance; with N(0,1) inputs the gradients are O(1), and an
+emulation of the kernels' roundings -- P and dS to bf16, D from the bf16
+output -- gives max-abs errors below 1e-2)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_25041_amd as ws
+from paper_2606_25041_amd import inputs
+from tests import gpu_support as gs
+
+pytestmark = pytest.mark.gpu
+
+
+def _grad_case(name, B, Hq, Hkv, D, lens, seed, text=None):
+    wl = inputs.prefill_workload(name, B, Hq, Hkv, D, lens, seed)
+    wl.text_starts = text
+    dout = inputs.bf16_normal(inputs.rng(seed, 9), tuple(wl.q.shape))
+    return wl, dout
+
+
+def _check(wl, dout):
+    gs.say(f"[gpu] bwd {wl.name}: B={wl.B} Hq={wl.Hq} Hkv={wl.Hkv} D={wl.D} L={wl.Lq}")
+    q, k, v = gs.to_dev_bf16(wl.q), gs.to_dev_bf16(wl.k), gs.to_dev_bf16(wl.v)
+    o, lse = ws.block_causal_prefill(q, k, v, wl.offsets, scale=wl.scale, want_lse=True,
+                                     text_starts=wl.text_starts)
+    dq, dk, dv = ws.block_causal_prefill_bwd(q, k, v, o, gs.to_dev_bf16(dout), lse, wl.offsets,
+                                             scale=wl.scale, text_starts=wl.text_starts)
+    torch.cuda.synchronize()
+    rq, rk, rv = oracle.prefill_bwd(inputs.bf16_bits(wl.q), inputs.bf16_bits(wl.k), inputs.bf16_bits(wl.v),
+                                    inputs.bf16_bits(dout), wl.offsets, wl.scale, text_starts=wl.text_starts)
+    for name, got, ref in (("dq", dq, rq), ("dk", dk, rk), ("dv", dv, rv)):
+        g = got.cpu().numpy().astype(np.float64)
+        assert np.all(np.isfinite(g)), name
+        err = np.abs(g - ref)
+        gs.say(f"[gpu]   {name}: max {err.max():.2e} mean {err.mean():.2e} (ref max {np.abs(ref).max():.2f})")
+        assert err.max() <= gs.MAX_ABS and err.mean() <= gs.MEAN_ABS, (name, err.max(), err.mean())
+    return dq, dk, dv
+
+
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("L,nb", [(777, 9), (300, 3)])
+def test_bwd_ragged_blocks(D, L, nb):
+    g = np.random.default_rng([L + D, 97])
+    lens = []
+    for _ in range(2):
+        cuts = np.sort(g.choice(np.arange(1, L), size=nb - 1, replace=False))
+        lens.append(np.diff(np.concatenate([[0], cuts, [L]])))
+    _check(*_grad_case(f"bwd_d{D}_L{L}", 2, 4, 2, D, lens, seed=81 + L + D))
+
+
+def test_bwd_unit_empty_and_long_blocks():
+    lens = [np.array([1, 1, 0, 5, 1, 200, 0, 1, 90, 60])]
+    _check(*_grad_case("bwd_unit_empty", 1, 2, 1, 128, lens, seed=83))
+
+
+def test_bwd_single_block_gqa4():
+    _check(*_grad_case("bwd_single", 1, 8, 2, 128, [np.array([333])], seed=85))
+
+
+def test_bwd_token_causal_segments():
+    g = inputs.rng(87, inputs.S_LENGTHS)
+    vis, aud, txt = inputs.interleaved_segments(g, 5)
+    wl, dout = _grad_case("bwd_text", 1, 4, 2, 128, [vis + aud + txt], seed=87)
+    wl.text_starts = inputs.text_starts_of(wl.offsets, txt[None])
+    _check(wl, dout)
+
+
+def test_bwd_all_causal_d64():
+    lens = [np.array([64, 1, 100, 35])]
+    wl, dout = _grad_case("bwd_all_causal", 1, 2, 2, 64, lens, seed=89)
+    wl.text_starts = wl.offsets[:, :-1].copy()
+    _check(wl, dout)
+
+
+def test_bwd_deterministic():
+    wl, dout = _grad_case("bwd_det", 1, 8, 2, 128, [np.array([100, 156, 256, 300])], seed=91)
+    q, k, v = gs.to_dev_bf16(wl.q), gs.to_dev_bf16(wl.k), gs.to_dev_bf16(wl.v)
+    o, lse = ws.block_causal_prefill(q, k, v, wl.offsets, want_lse=True)
+    d = gs.to_dev_bf16(dout)
+    gs.say("[gpu] bwd determinism")
+    a = ws.block_causal_prefill_bwd(q, k, v, o, d, lse, wl.offsets)
+    b = ws.block_causal_prefill_bwd(q, k, v, o, d, lse, wl.offsets)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
