@@ -367,6 +367,48 @@ def solver_loop_timing(dev, steps=8, reps=40):
     return out
 
 
+def backward_timing(dev, steps=5):
+    """Gradients of the whole-sequence workload (2 x 16384 tokens, GQA 32/8,
+    64 blocks of 256): dQ, dK and dV from dO, the forward's output and lse.
+    Algorithmic work 10 d flops per visible pair (recomputed S^T, dP, dV, dK,
+    dQ: 2.5 x the forward's), although the kernels recompute S and dP once
+    more (14 d)."""
+    wl = inputs.config(3)
+    q, k, v = wl.q.to(dev), wl.k.to(dev), wl.v.to(dev)
+    off = torch.from_numpy(wl.offsets.astype(np.int32))
+    offs = (off, off.to(dev))
+    o, lse = ws.block_causal_prefill(q, k, v, offs, want_lse=True)
+    g = torch.Generator(device=dev)
+    g.manual_seed(9200)
+    dout = torch.randn(tuple(q.shape), generator=g, device=dev).to(torch.bfloat16)
+    dq = torch.empty(tuple(q.shape), dtype=torch.float32, device=dev)
+    dk = torch.empty(tuple(k.shape), dtype=torch.float32, device=dev)
+    dv = torch.empty_like(dk)
+    work = torch.empty(ws.workspace_bytes(ws.WS_OP_PREFILL_BWD, wl.B, wl.Hq, wl.Hkv, wl.Lq, wl.Lq),
+                       dtype=torch.uint8, device=dev)
+
+    def run():
+        ws.block_causal_prefill_bwd(q, k, v, o, dout, lse, offs, dq=dq, dk=dk, dv=dv, workspace=work)
+
+    for _ in range(2):
+        run()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in ev:
+        a.record()
+        run()
+        b.record()
+    torch.cuda.synchronize()
+    ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+    flops = 2.5 * algorithmic_flops(wl)
+    tf = flops / (ms * 1e-3) / 1e12
+    log(f"[bench] prefill backward: {ms:.3f} ms, {tf:.0f} TFLOP/s")
+    out = {"workload": "prefill_bwd_b2_gqa32x8_d128_64x256", "ms": round(ms, 4), "TFLOP/s": round(tf, 1),
+           "mfma_frac": round(tf / BF16_PEAK_TFLOPS, 4), "flops": flops}
+    del q, k, v, o, lse, dout, dq, dk, dv, work
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(wl):
     """The fp64 oracle (as it stands) on the whole headline step."""
     import oracle  # test infrastructure: only this baseline leg uses it
@@ -470,6 +512,7 @@ def main():
 
     if not args.no_extra:
         extra.append(solver_loop_timing(dev))
+        extra.append(backward_timing(dev))
     sweeps = [] if (args.no_extra or args.no_sweep) else run_sweeps(dev, 200)
     cpu = None if args.no_cpu else cpu_baseline(wl)
     line = {

@@ -89,3 +89,29 @@ def test_bwd_deterministic():
     torch.cuda.synchronize()
     for x, y in zip(a, b):
         assert torch.equal(x, y)
+
+
+def test_bwd_full_size_prefill_closed_form():
+    """The whole-sequence workload (2 x 16384 tokens, GQA 32/8, 64 blocks of
+    256, K x 0.5) at full size, checked by a property that holds at any
+    size: rows of P sum to 1, so for every (stream, KV head) the dV of all
+    keys sums to the sum of dO over the group's rows and heads.  With P
+    rounded to bf16 (relative error <= 2^-9 per weight) the two sums differ
+    by at most 2^-9 (plus fp32 rounding) times the sum of |dO|."""
+    wl = inputs.config(3)
+    dout = inputs.bf16_normal(inputs.rng(93, 9), tuple(wl.q.shape))
+    q, k, v = gs.to_dev_bf16(wl.q), gs.to_dev_bf16(wl.k), gs.to_dev_bf16(wl.v)
+    gs.say("[gpu] bwd full-size prefill")
+    o, lse = ws.block_causal_prefill(q, k, v, wl.offsets, want_lse=True)
+    d = gs.to_dev_bf16(dout)
+    dq, dk, dv = ws.block_causal_prefill_bwd(q, k, v, o, d, lse, wl.offsets)
+    dq2, dk2, dv2 = ws.block_causal_prefill_bwd(q, k, v, o, d, lse, wl.offsets)
+    torch.cuda.synchronize()
+    for x, y in ((dq, dq2), (dk, dk2), (dv, dv2)):
+        assert torch.isfinite(x).all() and torch.equal(x, y)
+    G = wl.Hq // wl.Hkv
+    do64 = d.double().view(wl.B, wl.Lq, wl.Hkv, G, wl.D)
+    lhs = dv.double().sum(dim=1)                    # [B][Hkv][D]
+    rhs = do64.sum(dim=(1, 3))
+    bound = (2.0 ** -9 + 1e-5) * do64.abs().sum(dim=(1, 3)) + 1e-3
+    assert bool(((lhs - rhs).abs() <= bound).all()), float(((lhs - rhs).abs() - bound).max())
