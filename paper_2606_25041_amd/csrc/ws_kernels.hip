@@ -1011,14 +1011,34 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const BwdArgs a) {
     }
 }
 
+// Loads rows [r0, r0 + nrows) of a [rows][D] bf16 tile (row r of the tile
+// = global row min(r0 + r, rmax)) straight into LDS at `lds` in the
+// swizzled layout, spread over NWV waves: wave-wide load i of wave w fills
+// tile bytes [(i * NWV + w) * 1024, +1024), lane l the 16 bytes at +16 l,
+// so it fetches the chunk that belongs there.  The caller waits for them
+// (s_waitcnt vmcnt) before the barrier that publishes the tile.
+template <int D, int NWV, int ROWS>
+__device__ __forceinline__ void dma_rows(const char *g, int64_t st_bytes, int r0, int rmax, uint32_t lds,
+                                         int wave, int lane) {
+    constexpr int ROWB = 2 * D, RPW = 1024 / ROWB, LPR = ROWB / 16;
+    constexpr int NI = ROWS * ROWB / (NWV * 1024);
+    static_assert(NI >= 1 && ROWS * ROWB % (NWV * 1024) == 0, "the tile splits into wave-wide loads");
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+        const int r = (i * NWV + wave) * RPW + lane / LPR;
+        const int ch = (lane % LPR) ^ swz<D>(r);
+        const int gr = min(r0 + r, rmax);
+        dma16(g + (int64_t)gr * st_bytes + 16 * ch, lds + (i * NWV + wave) * 1024);
+    }
+}
+
 // dQ: one work-group = (stream, query head, 128 query rows), 4 waves x 32
-// rows; K/V tiles of 64 keys staged in LDS (two stages); tiles past the
-// last row's key end are never loaded.
+// rows; K/V tiles of 64 keys go straight to LDS (two stages); tiles past
+// the last row's key end are never loaded.
 template <int D>
 __global__ __launch_bounds__(256) void bwd_dq_kernel(const BwdArgs a) {
-    constexpr int ROWB = 2 * D, KK = D / 16, MD = D / 32, CPR = ROWB / 16;
+    constexpr int ROWB = 2 * D, KK = D / 16, MD = D / 32;
     constexpr int TILEB = 64 * ROWB;
-    constexpr int RPP = 256 / CPR, NP = 64 / RPP;
     __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * TILEB];   // [stage][K, V]
     const int nqt = (a.L + 127) / 128;
     const int wid = blockIdx.x;
@@ -1026,13 +1046,14 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(const BwdArgs a) {
     const int h = (wid / nqt) % a.Hq;
     const int b = wid / (nqt * a.Hq);
     const int g = h / a.G;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hf = lane >> 5, l32 = lane & 31;
+    const int tid = threadIdx.x, lane = tid & 63, hf = lane >> 5, l32 = lane & 31;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int q0 = qt * 128;
     const int row = q0 + 32 * wave + l32;
     const int rc = min(row, a.L - 1);
     const int32_t *kend_b = a.kend + (int64_t)b * a.L;
-    const int k_hi = kend_b[min(q0 + 127, a.L - 1)];
-    const int kfull = kend_b[q0];
+    const int k_hi = ld_uniform(kend_b, min(q0 + 127, a.L - 1));
+    const int kfull = ld_uniform(kend_b, q0);
     const int my_kend = kend_b[rc];
     const int64_t ridx = ((int64_t)b * a.Hq + h) * a.L + rc;
     const float lse2 = a.dl[2 * ridx], Dr = a.dl[2 * ridx + 1];
@@ -1049,26 +1070,13 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(const BwdArgs a) {
             dof[kk] = *(const bf16x8 *)(dp + 16 * kk);
         }
     }
-    const int lr = tid / CPR, lc = tid % CPR;
-    const uint16_t *kg = a.k + b * a.k_sb + g * a.k_sh + 8 * lc;
-    const uint16_t *vg = a.v + b * a.v_sb + g * a.v_sh + 8 * lc;
-    u32x4 kreg[NP], vreg[NP];
-    auto load_tile = [&](int t) {
-#pragma unroll
-        for (int p = 0; p < NP; ++p) {
-            const int key = min(t * 64 + lr + p * RPP, k_hi - 1);
-            kreg[p] = *(const u32x4 *)(kg + (int64_t)key * a.k_st);
-            vreg[p] = *(const u32x4 *)(vg + (int64_t)key * a.v_st);
-        }
-    };
-    auto store_tile = [&](int st) {
-        char *kt = smem + st * 2 * TILEB, *vt = kt + TILEB;
-#pragma unroll
-        for (int p = 0; p < NP; ++p) {
-            const int r = lr + p * RPP;
-            *(u32x4 *)(kt + tile_off<D>(r, lc)) = kreg[p];
-            *(u32x4 *)(vt + tile_off<D>(r, lc)) = vreg[p];
-        }
+    const char *kg = (const char *)(a.k + b * a.k_sb + g * a.k_sh);
+    const char *vg = (const char *)(a.v + b * a.v_sb + g * a.v_sh);
+    const int64_t kst = 2 * a.k_st, vst = 2 * a.v_st;
+    auto issue_tile = [&](int t) {
+        const uint32_t kl = lds_addr(smem) + (t & 1) * 2 * TILEB;
+        dma_rows<D, 4, 64>(kg, kst, t * 64, k_hi - 1, kl, wave, lane);
+        dma_rows<D, 4, 64>(vg, vst, t * 64, k_hi - 1, kl + TILEB, wave, lane);
     };
     const uint32_t kbase = (uint32_t)(l32 * ROWB + 16 * (hf ^ swz<D>(l32)));
     uint32_t tb[2];
@@ -1080,13 +1088,12 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(const BwdArgs a) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[md][v] = 0.f;
     const int ntile = (k_hi + 63) / 64;
-    if (ntile > 0) {
-        load_tile(0);
-        store_tile(0);
-    }
-    __syncthreads();
+    if (ntile > 0) issue_tile(0);
+    wait_vm_lgkm<0>();
+    wg_barrier();
     for (int t = 0; t < ntile; ++t) {
-        if (t + 1 < ntile) load_tile(t + 1);
+        // the other stage was last read before the previous barrier
+        if (t + 1 < ntile) issue_tile(t + 1);
         const char *kt = smem + (t & 1) * 2 * TILEB, *vt = kt + TILEB;
         f32x16 S[2], dPt[2];
 #pragma unroll
@@ -1121,8 +1128,8 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(const BwdArgs a) {
 #pragma unroll
             for (int md = 0; md < MD; ++md)
                 acc[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<D>(kt, tb, ks, md), dsf[ks], acc[md], 0, 0, 0);
-        if (t + 1 < ntile) store_tile((t + 1) & 1);
-        __syncthreads();
+        wait_vm_lgkm<0>();   // tile t + 1 landed (and this tile's LDS reads are done)
+        wg_barrier();
     }
     if (row < a.L) {
         float *op = a.dq + b * a.dq_sb + (int64_t)row * a.dq_st + h * a.dq_sh;
@@ -1138,31 +1145,37 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(const BwdArgs a) {
     }
 }
 
-// dK and dV: one work-group = (stream, KV head, 128 keys), 4 waves x 32
-// keys.  The work-group's K and V stay in LDS; for every query head of the
-// KV group, chunks of 32 query rows (from the first row that sees any of
-// these keys) are staged in LDS (two stages) with their (lse, D) and key
-// ends.
+// dK and dV: one work-group = (stream, KV head, 128 keys), 8 waves: wave w
+// owns keys 32 (w % 4) .. + 31 and belongs to group w / 4.  The
+// work-group's K and V stay in LDS; the chunks of 32 query rows (from the
+// first row that sees any of these keys, for every query head of the KV
+// group) alternate between the two groups, each with its own two LDS
+// stages, so two waves share every SIMD.  At the end group 1 hands its
+// partial sums to group 0 through LDS (fixed order: group 0's + group 1's).
 template <int D>
-__global__ __launch_bounds__(256) void bwd_dkdv_kernel(const BwdArgs a) {
-    constexpr int ROWB = 2 * D, KK = D / 16, MD = D / 32, CPR = ROWB / 16;
+__global__ __launch_bounds__(512) void bwd_dkdv_kernel(const BwdArgs a) {
+    constexpr int ROWB = 2 * D, KK = D / 16, MD = D / 32;
     constexpr int TILEK = 128 * ROWB, TILEC = 32 * ROWB;
-    constexpr int RPP = 256 / CPR, NPK = 128 / RPP, NPC = 32 / RPP;
-    __shared__ __attribute__((aligned(1024))) char smem[2 * TILEK + 2 * 2 * TILEC];
-    __shared__ __attribute__((aligned(16))) float sdl[2][2][32];   // [stage][lse2, D][row]
-    __shared__ __attribute__((aligned(16))) int skend[2][32];
+    constexpr int CPR = ROWB / 16, RPP = 512 / CPR, NPK = 128 / RPP;
+    constexpr int SMEM = 2 * TILEK + 2 * 2 * 2 * TILEC;   // K, V; [group][stage][Q, dO]
+    static_assert(2 * 4 * MD * 16 * 64 * 4 <= SMEM, "the partial sums fit the tiles' space");
+    __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+    __shared__ __attribute__((aligned(16))) float sdl[2][2][2][32];   // [group][stage][lse2, D][row]
+    __shared__ __attribute__((aligned(16))) int skend[2][2][32];
     const int nkt = (a.L + 127) / 128;
     const int wid = blockIdx.x;
     const int kt = wid % nkt;
     const int kvh = (wid / nkt) % a.Hkv;
     const int b = wid / (nkt * a.Hkv);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hf = lane >> 5, l32 = lane & 31;
+    const int tid = threadIdx.x, lane = tid & 63, hf = lane >> 5, l32 = lane & 31;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int grp = wave >> 2, sub = wave & 3, gtid = tid & 255;
     const int kw0 = kt * 128;
-    const int key = kw0 + 32 * wave + l32;
-    const int lr = tid / CPR, lc = tid % CPR;
+    const int key = kw0 + 32 * sub + l32;
     const float c2 = a.scale_log2;
     // the work-group's K and V (rows past the end repeat the last key)
     {
+        const int lr = tid / CPR, lc = tid % CPR;
         const uint16_t *kg = a.k + b * a.k_sb + kvh * a.k_sh + 8 * lc;
         const uint16_t *vg = a.v + b * a.v_sb + kvh * a.v_sh + 8 * lc;
 #pragma unroll
@@ -1182,49 +1195,42 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(const BwdArgs a) {
     }
     const int i0 = lo;
     const int nch = (a.L - i0 + 31) / 32;
-    const int total = a.G * nch;
+    const int total = a.G * nch;            // chunks; group grp takes chunks grp, grp + 2, ...
+    const int nstep = (total + 1) / 2;
 
-    u32x4 qreg[NPC], dreg[NPC];
-    float lreg = 0.f, dreg1 = 0.f;
-    int kreg1 = 0;
-    auto load_chunk = [&](int it) {
+    float lreg = 0.f, dreg = 0.f;
+    int kreg = 0;
+    auto chunk_base = [&](int it) -> uint32_t { return (uint32_t)(2 * TILEK + ((grp * 2 + (it >> 1 & 1)) * 2) * TILEC); };
+    // the DMA of chunk it (Q and dO rows) and the (lse2, D, key end) of its
+    // rows into registers; group-uniform
+    auto issue_chunk = [&](int it) {
         const int hh = it / nch, ch = it - hh * nch;
         const int h = kvh * a.G + hh;
         const int r0 = i0 + 32 * ch;
-        const uint16_t *qg = a.q + b * a.q_sb + h * a.q_sh + 8 * lc;
-        const uint16_t *dg = a.dout + b * a.do_sb + h * a.do_sh + 8 * lc;
-#pragma unroll
-        for (int p = 0; p < NPC; ++p) {
-            const int r = min(r0 + lr + p * RPP, a.L - 1);
-            qreg[p] = *(const u32x4 *)(qg + (int64_t)r * a.q_st);
-            dreg[p] = *(const u32x4 *)(dg + (int64_t)r * a.do_st);
-        }
-        if (tid < 32) {
-            const int r = r0 + tid;
+        const uint32_t base = lds_addr(smem) + chunk_base(it);
+        dma_rows<D, 4, 32>((const char *)(a.q + b * a.q_sb + h * a.q_sh), 2 * a.q_st, r0, a.L - 1, base, sub, lane);
+        dma_rows<D, 4, 32>((const char *)(a.dout + b * a.do_sb + h * a.do_sh), 2 * a.do_st, r0, a.L - 1,
+                           base + TILEC, sub, lane);
+        if (gtid < 32) {
+            const int r = r0 + gtid;
             if (r < a.L) {
                 const int64_t idx = ((int64_t)b * a.Hq + h) * a.L + r;
                 lreg = a.dl[2 * idx];
-                dreg1 = a.dl[2 * idx + 1];
-                kreg1 = kend_b[r];
+                dreg = a.dl[2 * idx + 1];
+                kreg = kend_b[r];
             } else {
                 lreg = 0.f;
-                dreg1 = 0.f;
-                kreg1 = 0;   // no key visible
+                dreg = 0.f;
+                kreg = 0;   // no key visible
             }
         }
     };
-    auto store_chunk = [&](int st) {
-        char *qt = smem + 2 * TILEK + st * 2 * TILEC, *dt = qt + TILEC;
-#pragma unroll
-        for (int p = 0; p < NPC; ++p) {
-            const int r = lr + p * RPP;
-            *(u32x4 *)(qt + tile_off<D>(r, lc)) = qreg[p];
-            *(u32x4 *)(dt + tile_off<D>(r, lc)) = dreg[p];
-        }
-        if (tid < 32) {
-            sdl[st][0][tid] = lreg;
-            sdl[st][1][tid] = dreg1;
-            skend[st][tid] = kreg1;
+    auto store_rowinfo = [&](int it) {
+        if (gtid < 32) {
+            const int st = it >> 1 & 1;
+            sdl[grp][st][0][gtid] = lreg;
+            sdl[grp][st][1][gtid] = dreg;
+            skend[grp][st][gtid] = kreg;
         }
     };
     const uint32_t kbase = (uint32_t)(l32 * ROWB + 16 * (hf ^ swz<D>(l32)));
@@ -1236,58 +1242,80 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(const BwdArgs a) {
     for (int md = 0; md < MD; ++md)
 #pragma unroll
         for (int v = 0; v < 16; ++v) dk[md][v] = dv[md][v] = 0.f;
-    if (total > 0) {
-        load_chunk(0);
-        store_chunk(0);
+    if (grp < total) {
+        issue_chunk(grp);
+        store_rowinfo(grp);
     }
-    __syncthreads();
-    const char *ktile = smem + 32 * wave * ROWB, *vtile = smem + TILEK + 32 * wave * ROWB;
-    for (int it = 0; it < total; ++it) {
-        const int st = it & 1;
-        if (it + 1 < total) load_chunk(it + 1);
-        const char *qt = smem + 2 * TILEK + st * 2 * TILEC, *dt = qt + TILEC;
-        // S = Q K^T and dP = dO V^T: query rows x this wave's 32 keys
-        f32x16 S, dP;
+    wait_vm_lgkm<0>();
+    wg_barrier();
+    const char *ktile = smem + 32 * sub * ROWB, *vtile = smem + TILEK + 32 * sub * ROWB;
+    for (int s = 0; s < nstep; ++s) {
+        const int it = 2 * s + grp;          // this group's chunk
+        const int nx = it + 2;               // its next one (other stage)
+        if (nx < total) issue_chunk(nx);
+        if (it < total) {
+            const int st = it >> 1 & 1;
+            const char *qt = smem + chunk_base(it), *dt = qt + TILEC;
+            // S = Q K^T and dP = dO V^T: query rows x this wave's 32 keys
+            f32x16 S, dP;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) S[v] = dP[v] = 0.f;
+            for (int v = 0; v < 16; ++v) S[v] = dP[v] = 0.f;
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-            const bf16x8 qa = *(const bf16x8 *)(qt + (kbase ^ (32 * kk)));
-            const bf16x8 kb = *(const bf16x8 *)(ktile + (kbase ^ (32 * kk)));
-            S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kb, S, 0, 0, 0);
-            const bf16x8 da = *(const bf16x8 *)(dt + (kbase ^ (32 * kk)));
-            const bf16x8 vb = *(const bf16x8 *)(vtile + (kbase ^ (32 * kk)));
-            dP = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vb, dP, 0, 0, 0);
-        }
-        // the lane's 16 query rows 8 (v / 4) + 4 hf + v % 4
-        bf16x8 pf[2], dsf[2];
-#pragma unroll
-        for (int gq = 0; gq < 4; ++gq) {
-            const f32x4 l4 = *(const f32x4 *)&sdl[st][0][8 * gq + 4 * hf];
-            const f32x4 d4 = *(const f32x4 *)&sdl[st][1][8 * gq + 4 * hf];
-            const int4 k4 = *(const int4 *)&skend[st][8 * gq + 4 * hf];
-            const int ke[4] = {k4.x, k4.y, k4.z, k4.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int v = 4 * gq + e;
-                const float p0 = fast_exp2(__builtin_fmaf(S[v], c2, -l4[e]));
-                const float p = key < ke[e] ? p0 : 0.f;
-                pf[v >> 3][v & 7] = (__bf16)p;
-                dsf[v >> 3][v & 7] = (__bf16)(p * (dP[v] - d4[e]));
+            for (int kk = 0; kk < KK; ++kk) {
+                const bf16x8 qa = *(const bf16x8 *)(qt + (kbase ^ (32 * kk)));
+                const bf16x8 kb = *(const bf16x8 *)(ktile + (kbase ^ (32 * kk)));
+                S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kb, S, 0, 0, 0);
+                const bf16x8 da = *(const bf16x8 *)(dt + (kbase ^ (32 * kk)));
+                const bf16x8 vb = *(const bf16x8 *)(vtile + (kbase ^ (32 * kk)));
+                dP = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da, vb, dP, 0, 0, 0);
             }
-        }
-        // dV^T += dO^T P and dK^T += Q^T dS
+            // the lane's 16 query rows 8 (v / 4) + 4 hf + v % 4
+            bf16x8 pf[2], dsf[2];
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
+            for (int gq = 0; gq < 4; ++gq) {
+                const f32x4 l4 = *(const f32x4 *)&sdl[grp][st][0][8 * gq + 4 * hf];
+                const f32x4 d4 = *(const f32x4 *)&sdl[grp][st][1][8 * gq + 4 * hf];
+                const int4 k4 = *(const int4 *)&skend[grp][st][8 * gq + 4 * hf];
+                const int ke[4] = {k4.x, k4.y, k4.z, k4.w};
 #pragma unroll
-            for (int md = 0; md < MD; ++md) {
-                dv[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<D>(dt, tb, ks, md), pf[ks], dv[md], 0, 0, 0);
-                dk[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<D>(qt, tb, ks, md), dsf[ks], dk[md], 0, 0, 0);
+                for (int e = 0; e < 4; ++e) {
+                    const int v = 4 * gq + e;
+                    const float p0 = fast_exp2(__builtin_fmaf(S[v], c2, -l4[e]));
+                    const float p = key < ke[e] ? p0 : 0.f;
+                    pf[v >> 3][v & 7] = (__bf16)p;
+                    dsf[v >> 3][v & 7] = (__bf16)(p * (dP[v] - d4[e]));
+                }
             }
-        if (it + 1 < total) store_chunk((it + 1) & 1);
-        __syncthreads();
+            // dV^T += dO^T P and dK^T += Q^T dS
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+                for (int md = 0; md < MD; ++md) {
+                    dv[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<D>(dt, tb, ks, md), pf[ks], dv[md], 0, 0, 0);
+                    dk[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<D>(qt, tb, ks, md), dsf[ks], dk[md], 0, 0, 0);
+                }
+        }
+        // the row data of the next chunk goes to the other stage, which was
+        // last read before the previous barrier
+        if (nx < total) store_rowinfo(nx);
+        wait_vm_lgkm<0>();   // the next chunks landed; this step's LDS reads are done
+        wg_barrier();
     }
-    if (key < a.L) {
+    // group 1 -> LDS -> group 0, in register order (conflict-free)
+    float *part = (float *)smem;
+    const int pbase = (sub * MD) * 16 * 64 + lane;
+    if (grp == 1) {
+#pragma unroll
+        for (int md = 0; md < MD; ++md)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                part[pbase + (md * 16 + v) * 64] = dk[md][v];
+                part[4 * MD * 16 * 64 + pbase + (md * 16 + v) * 64] = dv[md][v];
+            }
+    }
+    wait_vm_lgkm<0>();
+    wg_barrier();
+    if (grp == 0 && key < a.L) {
         float *kp = a.dk + b * a.dk_sb + (int64_t)key * a.dk_st + kvh * a.dk_sh;
         float *vp = a.dv + b * a.dv_sb + (int64_t)key * a.dv_st + kvh * a.dv_sh;
 #pragma unroll
@@ -1297,8 +1325,9 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(const BwdArgs a) {
                 f32x4 kv, vv;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    kv[e] = dk[md][4 * gq + e] * a.scale;
-                    vv[e] = dv[md][4 * gq + e];
+                    const int v = 4 * gq + e;
+                    kv[e] = (dk[md][v] + part[pbase + (md * 16 + v) * 64]) * a.scale;
+                    vv[e] = dv[md][v] + part[4 * MD * 16 * 64 + pbase + (md * 16 + v) * 64];
                 }
                 *(f32x4 *)(kp + 32 * md + 8 * gq + 4 * hf) = kv;
                 *(f32x4 *)(vp + 32 * md + 8 * gq + 4 * hf) = vv;
@@ -1315,7 +1344,7 @@ int launch_bwd_t(const BwdArgs &a, hipStream_t st) {
     const int64_t nqt = (a.L + 127) / 128;
     hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3((unsigned)(a.B * a.Hq * nqt)), dim3(256), 0, st, a);
     if (int e = (int)hipGetLastError()) return e;
-    hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3((unsigned)(a.B * a.Hkv * nqt)), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3((unsigned)(a.B * a.Hkv * nqt)), dim3(512), 0, st, a);
     return (int)hipGetLastError();
 }
 
