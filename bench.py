@@ -448,6 +448,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-sweep", action="store_true", help="skip the KV-length sweeps")
     ap.add_argument("--config", type=int, default=2, help="headline workload index (1-5)")
+    ap.add_argument("--bwd-only", action="store_true",
+                    help="only time the gradients of the whole-sequence workload (for profiling)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (to calibrate "
                          "the FETCH_SIZE / WRITE_SIZE counters against known bytes)")
@@ -471,6 +473,9 @@ def main():
         sys.exit(1)
     dev = torch.device("cuda:0")
     ws.library()
+    if args.bwd_only:
+        print(json.dumps(backward_timing(dev, steps=args.steps)), flush=True)
+        return
 
     wl = inputs.config(args.config)
     if wl.kind == "step" and args.config == 2:
