@@ -1,11 +1,14 @@
 // gfx950 (MI355X) kernels for block-causal streaming attention.
 //
 // Block-causal rule (Wan-Streamer v0.1, Abstract; Sec. 1 with Fig. 1): a
-// token sees its whole own block and every earlier block.  The step kernel
-// runs the performer's current unit against its full-history cache
-// (Sec. 2.4); the prefill kernel covers whole sequences (Sec. 2.4, system
-// prefill); the append kernel commits a KV slice to the paged cache
-// (Sec. 2.4).
+// token sees its whole own block and every earlier block; a block may end in
+// a token-causal segment (the thinker's language and state slots, Sec. 1 and
+// Sec. 2.4) whose tokens see the segment only up to themselves.  The step
+// kernel runs the current unit against its full-history cache (Sec. 2.4);
+// the prefill kernel covers whole sequences (Sec. 2.4, system prefill); the
+// append kernel commits a KV slice to the paged cache (Sec. 2.4); the
+// gradient kernels at the end of the file serve training, which uses the
+// same causal format (Sec. 2.3).
 //
 // Attention kernel design (one work-group = one (stream, query head,
 // query tile, KV split) work item; 8 waves x 32 query rows = 256 rows):
