@@ -200,7 +200,10 @@ def time_workload(wl, steps, warmup, dev, rotate=True, latency_steps=None):
         cases[i % copies].run()
         ev[i][1].record()
     torch.cuda.synchronize()
-    lat = float(np.median([a.elapsed_time(b) for a, b in ev])) if n_lat else ev_ms
+    lats = [a.elapsed_time(b) for a, b in ev]
+    lat = float(np.median(lats)) if n_lat else ev_ms
+    time_workload.percentiles = ((float(np.percentile(lats, 10)), float(np.percentile(lats, 90)))
+                                 if n_lat else (ev_ms, ev_ms))
     log(f"[bench] {wl.name}: wall {wall_ms:.4f} ms/step, events over the timed region {ev_ms:.4f} "
         f"ms/step, per-step latency median {lat:.4f} ms")
     return wall_ms, ev_ms, lat, cases[0]
@@ -483,6 +486,7 @@ def main():
     flops, nbytes = algorithmic_flops(wl), algorithmic_bytes(wl)
     torch.cuda.synchronize()
     wall_ms, ev_mean, ev_med, _ = time_workload(wl, args.steps, args.warmup, dev)
+    lat_p10, lat_p90 = time_workload.percentiles
     tflops = flops / (wall_ms * 1e-3) / 1e12
     gbs_kernel = nbytes / (ev_mean * 1e-3) / 1e9
     ai = flops / nbytes
@@ -539,6 +543,7 @@ def main():
                    "page_size": 64, "fused_append": bool(wl.fuse_append), "seed": wl.seed,
                    "parallelism": "none (1 GPU)"},
         "latency_ms_per_block": round(ev_med, 5),
+        "latency_ms_p10_p90": [round(lat_p10, 5), round(lat_p90, 5)],
         "roofline": roof,
         "cpu_baseline": cpu,
         "extra": extra,

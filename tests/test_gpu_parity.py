@@ -137,6 +137,7 @@ def _sampled(wl, cache, must, n=48, seed=5):
 
 def test_config2_step_full_size():
     wl = inputs.config(2)
+    wl.fuse_append = True   # as the benchmark runs it (the block is committed in the same launch)
     cache = gs.device_cache(wl, wl.cache_lens, fill_on_gpu=True)
     _sampled(wl, cache, must=[(0, 0, 0), (0, 23, 255), (0, 11, 128), (0, 5, 63)])
 
