@@ -168,7 +168,7 @@ class DeviceCase:
                                     lse=self.lse, want_lse=True, text_starts=self.text)
 
 
-def time_workload(wl, steps, warmup, dev, rotate=True, latency_steps=None):
+def time_workload(wl, steps, warmup, dev, rotate=True, latency_steps=None, stats=None):
     """Returns (ms per step from the synchronised wall clock over the K timed
     steps, ms per step from HIP events recorded on the launch stream at the
     two ends of the same timed region, median per-step latency in ms, one
@@ -202,8 +202,9 @@ def time_workload(wl, steps, warmup, dev, rotate=True, latency_steps=None):
     torch.cuda.synchronize()
     lats = [a.elapsed_time(b) for a, b in ev]
     lat = float(np.median(lats)) if n_lat else ev_ms
-    time_workload.percentiles = ((float(np.percentile(lats, 10)), float(np.percentile(lats, 90)))
-                                 if n_lat else (ev_ms, ev_ms))
+    if stats is not None:   # p10 / p90 of the per-step latency
+        stats["p10"] = float(np.percentile(lats, 10)) if n_lat else ev_ms
+        stats["p90"] = float(np.percentile(lats, 90)) if n_lat else ev_ms
     log(f"[bench] {wl.name}: wall {wall_ms:.4f} ms/step, events over the timed region {ev_ms:.4f} "
         f"ms/step, per-step latency median {lat:.4f} ms")
     return wall_ms, ev_ms, lat, cases[0]
@@ -485,8 +486,8 @@ def main():
         wl.fuse_append = True  # the per-block step commits its block
     flops, nbytes = algorithmic_flops(wl), algorithmic_bytes(wl)
     torch.cuda.synchronize()
-    wall_ms, ev_mean, ev_med, _ = time_workload(wl, args.steps, args.warmup, dev)
-    lat_p10, lat_p90 = time_workload.percentiles
+    lat_stats = {}
+    wall_ms, ev_mean, ev_med, _ = time_workload(wl, args.steps, args.warmup, dev, stats=lat_stats)
     tflops = flops / (wall_ms * 1e-3) / 1e12
     gbs_kernel = nbytes / (ev_mean * 1e-3) / 1e9
     ai = flops / nbytes
@@ -543,7 +544,7 @@ def main():
                    "page_size": 64, "fused_append": bool(wl.fuse_append), "seed": wl.seed,
                    "parallelism": "none (1 GPU)"},
         "latency_ms_per_block": round(ev_med, 5),
-        "latency_ms_p10_p90": [round(lat_p10, 5), round(lat_p90, 5)],
+        "latency_ms_p10_p90": [round(lat_stats["p10"], 5), round(lat_stats["p90"], 5)],
         "roofline": roof,
         "cpu_baseline": cpu,
         "extra": extra,
