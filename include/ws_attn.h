@@ -183,6 +183,10 @@ int ws_kv_append(const ws_paged_kv *kv, int32_t batch,
  *                bytes (NULL allowed when that is 0); its contents on entry
  *                are ignored.
  * new_len x (num_q_heads / num_kv_heads) must not exceed 2^30 (WS_ERR_SHAPE).
+ * The library splits long caches into KV partitions merged by a second
+ * launch; the environment variable WS_SPLITS (1..32), read at each call,
+ * overrides the chosen partition count (for tuning; ws_workspace_bytes
+ * follows the same setting, so read both under the same environment).
  * Errors: WS_ERR_NULL, WS_ERR_SHAPE, WS_ERR_UNSUPPORTED, WS_ERR_ALIGN,
  * WS_ERR_HEADS, WS_ERR_CAPACITY, WS_ERR_PAGE, WS_ERR_WORKSPACE, WS_ERR_HIP.
  */
