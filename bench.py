@@ -274,11 +274,12 @@ class SweepCase:
                                  workspace=self.workspace, text_starts=self.text)
 
 
-def run_sweeps(dev, steps):
+def run_sweeps(dev, steps, points=None):
     """Median HIP-event time per point, over device copies rotated so that
     more than the 256 MB last-level cache is touched between reuses."""
+    todo = SWEEPS if points is None else points
     points = []
-    for i, pt in enumerate(SWEEPS):
+    for i, pt in enumerate(todo):
         nbytes = algorithmic_bytes(pt)
         copies = min(64, max(1, math.ceil(ROTATE_BYTES / nbytes)))
         cases = [SweepCase(pt, dev, 7000 + 100 * i + c) for c in range(copies)]
@@ -452,6 +453,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-sweep", action="store_true", help="skip the KV-length sweeps")
     ap.add_argument("--config", type=int, default=2, help="headline workload index (1-5)")
+    ap.add_argument("--sweep-only", default=None, metavar="NAME",
+                    help="only time the named KV-length sweep point(s), comma-separated (for profiling)")
     ap.add_argument("--bwd-only", action="store_true",
                     help="only time the gradients of the whole-sequence workload (for profiling)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -479,6 +482,14 @@ def main():
     ws.library()
     if args.bwd_only:
         print(json.dumps(backward_timing(dev, steps=args.steps)), flush=True)
+        return
+    if args.sweep_only:
+        names = set(args.sweep_only.split(","))
+        pts = [p for p in SWEEPS if p.name in names]
+        if not pts:
+            print(f"no sweep point named {args.sweep_only}", file=sys.stderr)
+            sys.exit(2)
+        print(json.dumps(run_sweeps(dev, args.steps, points=pts)), flush=True)
         return
 
     wl = inputs.config(args.config)
