@@ -54,6 +54,8 @@ def _bind(lib):
     lib.wso_prefill_text.restype = I
     lib.wso_step_text.argtypes = [P, P, P, P, P, I, I, I, I, P, P, I, I, I, D, P, I64, P, P, P, I]
     lib.wso_step_text.restype = I
+    lib.wso_step_varlen.argtypes = [P, P, P, P, P, I, I, I, I, P, P, P, I, I, I, D, P, I64, P, P, P, I]
+    lib.wso_step_varlen.restype = I
     lib.wso_prefill_bwd.argtypes = [P, P, P, P, I, I, I, I, I, I, P, I, P, D, P, P, P, I]
     lib.wso_prefill_bwd.restype = I
     lib.wso_mutant.restype = I
@@ -125,11 +127,12 @@ def prefill(q, k, v, offsets, scale, rows=None, want_probs=False, nthreads=None,
 
 
 def step(q, k_cache, v_cache, cache_lens, k_new, v_new, scale, rows=None,
-         want_probs=False, nthreads=None, lib=None, text_starts=None):
+         want_probs=False, nthreads=None, lib=None, text_starts=None, new_lens=None):
     """One streaming step: the new block attends to its stream's cache
     (tokens [0, cache_lens[b])) and bidirectionally to itself, except for an
     optional token-causal segment starting at text_starts[b] within the
-    block (Lq: none).
+    block (Lq: none).  new_lens (optional, [B], 1..Lq): stream b's block has
+    new_lens[b] tokens; the rest of its Lq positions are padding, never keys.
 
     q: [B][Lq][Hq][d]; k_cache, v_cache: [B][Lc_max][Hkv][d] logical cache;
     k_new, v_new: [B][Lq][Hkv][d].  Returns like ``prefill``; probs rows have
@@ -161,10 +164,13 @@ def step(q, k_cache, v_cache, cache_lens, k_new, v_new, scale, rows=None,
     ts = None
     if text_starts is not None:
         ts = np.ascontiguousarray(np.asarray(text_starts, dtype=np.int32).reshape(B))
-    rc = lib.wso_step_text(_ptr(q), _ptr(kc), _ptr(vc), _ptr(kn), _ptr(vn), dt,
-                           B, Lq, Lc_max, _ptr(lens), _ptr(ts), Hq, Hkv, d, float(scale),
-                           _ptr(rows_a), n, _ptr(out), _ptr(lse), _ptr(probs),
-                           int(nthreads or default_threads()))
+    nl = None
+    if new_lens is not None:
+        nl = np.ascontiguousarray(np.asarray(new_lens, dtype=np.int32).reshape(B))
+    rc = lib.wso_step_varlen(_ptr(q), _ptr(kc), _ptr(vc), _ptr(kn), _ptr(vn), dt,
+                             B, Lq, Lc_max, _ptr(lens), _ptr(nl), _ptr(ts), Hq, Hkv, d, float(scale),
+                             _ptr(rows_a), n, _ptr(out), _ptr(lse), _ptr(probs),
+                             int(nthreads or default_threads()))
     if rc != 0:
         raise ValueError(f"oracle step rejected its arguments (rc={rc})")
     return (out, lse, probs) if want_probs else (out, lse)

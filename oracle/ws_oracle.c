@@ -103,6 +103,9 @@ typedef struct {
      * prefill: [B][nb] absolute positions; step: [B] positions within the
      * new block */
     const int32_t *text_starts;
+    /* step only: tokens of stream b's new block (<= Lq), or NULL for Lq;
+     * tokens past it are padding: never keys */
+    const int32_t *new_lens;
     /* row list: nrows triples (b, h, i); NULL means every row */
     const int32_t *rows;
     int64_t nrows;
@@ -181,6 +184,12 @@ static void wso_mask_row(const wso_job *J, int b, int64_t i, unsigned char *mask
 #else
         int vis = beta_k <= beta_q;
 #endif
+#if WSO_MUTANT == 13
+        if (J->kind == WSO_STEP && J->new_lens && j > (int64_t)J->cache_lens[b] + J->new_lens[b])
+#else
+        if (J->kind == WSO_STEP && J->new_lens && j >= (int64_t)J->cache_lens[b] + J->new_lens[b])
+#endif
+            vis = 0;   /* padding of the new block */
         if (vis && beta_k == beta_q && tau >= 0) {
             /* same block: a key of the segment is visible only to segment
              * queries at or after it */
@@ -466,14 +475,17 @@ int wso_prefill(const void *q, const void *k, const void *v, int dtype,
  * Lc_max + Lq (entries past the stream's own key count are left untouched).
  * text_starts: NULL, or [B] start of the new block's token-causal segment
  * within the block (0 <= text_starts[b] <= Lq; Lq: no segment).
+ * new_lens: NULL, or [B] tokens of each stream's new block (1..Lq); the
+ * block's tokens past new_lens[b] are padding and never keys (their own
+ * rows are computed by the same rule).
  */
-int wso_step_text(const void *q, const void *kc, const void *vc,
-                  const void *kn, const void *vn, int dtype,
-                  int B, int Lq, int Lc_max, const int32_t *cache_lens,
-                  const int32_t *text_starts,
-                  int Hq, int Hkv, int d, double scale,
-                  const int32_t *rows, int64_t nrows,
-                  double *out, double *lse, double *probs, int nthreads)
+int wso_step_varlen(const void *q, const void *kc, const void *vc,
+                    const void *kn, const void *vn, int dtype,
+                    int B, int Lq, int Lc_max, const int32_t *cache_lens,
+                    const int32_t *new_lens, const int32_t *text_starts,
+                    int Hq, int Hkv, int d, double scale,
+                    const int32_t *rows, int64_t nrows,
+                    double *out, double *lse, double *probs, int nthreads)
 {
     if (wso_check_common(B, Lq, Hq, Hkv, d) || Lc_max < 0 || !cache_lens || !out)
         return -2;
@@ -481,6 +493,8 @@ int wso_step_text(const void *q, const void *kc, const void *vc,
         if (cache_lens[b] < 0 || cache_lens[b] > Lc_max)
             return -2;
         if (text_starts && (text_starts[b] < 0 || text_starts[b] > Lq))
+            return -2;
+        if (new_lens && (new_lens[b] < 1 || new_lens[b] > Lq))
             return -2;
     }
     wso_job J;
@@ -495,6 +509,7 @@ int wso_step_text(const void *q, const void *kc, const void *vc,
     J.vc = (wso_view){vc, dtype, (int64_t)Lc_max * Hkv * d, (int64_t)Hkv * d, d};
     J.cache_lens = cache_lens;
     J.text_starts = text_starts;
+    J.new_lens = new_lens;
     J.rows = rows;
     J.nrows = nrows;
     J.out = out;
@@ -502,6 +517,19 @@ int wso_step_text(const void *q, const void *kc, const void *vc,
     J.probs = rows ? probs : NULL;
     J.lk_max = (int64_t)Lc_max + Lq;
     return wso_run(&J, nthreads);
+}
+
+/* Equal new-block lengths (new_lens = NULL). */
+int wso_step_text(const void *q, const void *kc, const void *vc,
+                  const void *kn, const void *vn, int dtype,
+                  int B, int Lq, int Lc_max, const int32_t *cache_lens,
+                  const int32_t *text_starts,
+                  int Hq, int Hkv, int d, double scale,
+                  const int32_t *rows, int64_t nrows,
+                  double *out, double *lse, double *probs, int nthreads)
+{
+    return wso_step_varlen(q, kc, vc, kn, vn, dtype, B, Lq, Lc_max, cache_lens, NULL, text_starts, Hq, Hkv,
+                           d, scale, rows, nrows, out, lse, probs, nthreads);
 }
 
 /* The same with no token-causal segment in the new block. */

@@ -528,6 +528,35 @@ def pin_bwd_later_block_keeps_earlier_dq(lib):
     assert np.array_equal(dq1, dq2[:, :L])
 
 
+def pin_step_varlen_is_truncated_block(lib):
+    """A step whose new blocks are padded to a common length equals, row for
+    row, the step over each stream's real tokens only (bitwise): padding is
+    never a key.  With a token-causal segment as well."""
+    rng = _rng(45)
+    B, Lq, Lc, H, Hkv, d = 3, 7, 9, 4, 2, 5
+    q = rng.standard_normal((B, Lq, H, d))
+    kc, vc = (rng.standard_normal((B, Lc, Hkv, d)) for _ in range(2))
+    kn, vn = (rng.standard_normal((B, Lq, Hkv, d)) for _ in range(2))
+    lens, new_lens, ts = [9, 0, 4], [7, 3, 1], [7, 1, 0]
+    for text in (None, ts):
+        o, l = oracle.step(q, kc, vc, lens, kn, vn, 0.6, lib=lib, new_lens=new_lens, text_starts=text)
+        for b in range(B):
+            n = new_lens[b]
+            tb = None if text is None else [min(text[b], n)]
+            o1, l1 = oracle.step(q[b:b + 1, :n], kc[b:b + 1], vc[b:b + 1], [lens[b]], kn[b:b + 1, :n],
+                                 vn[b:b + 1, :n], 0.6, lib=lib, text_starts=tb)
+            assert np.array_equal(o[b:b + 1, :n], o1), (b, text)
+            assert np.array_equal(l[b:b + 1, :, :n], l1), (b, text)
+    # padding values never matter (poisoned: same results)
+    kn2, vn2 = kn.copy(), vn.copy()
+    for b, n in enumerate(new_lens):
+        kn2[b, n:] = 1e6
+        vn2[b, n:] = np.nan
+    o2, l2 = oracle.step(q, kc, vc, lens, kn2, vn2, 0.6, lib=lib, new_lens=new_lens)
+    o3, l3 = oracle.step(q, kc, vc, lens, kn, vn, 0.6, lib=lib, new_lens=new_lens)
+    assert np.array_equal(o2, o3) and np.array_equal(l2, l3)
+
+
 ALL_PINS = [
     pin_bruteforce_all_compositions,
     pin_single_block_is_full_attention,
@@ -552,6 +581,7 @@ ALL_PINS = [
     pin_bwd_finite_differences,
     pin_bwd_closed_forms,
     pin_bwd_later_block_keeps_earlier_dq,
+    pin_step_varlen_is_truncated_block,
 ]
 
 # the deliberately broken oracle builds (see WSO_MUTANT in ws_oracle.c)
@@ -568,4 +598,5 @@ MUTANTS = {
     10: "observation tokens see their block's segment",
     11: "gradient: D_i term dropped from dS",
     12: "gradient: scale dropped from dK",
+    13: "first padding token of a short new block used as a key",
 }
