@@ -75,7 +75,7 @@
 extern "C" {
 #endif
 
-#define WS_ABI_VERSION 3
+#define WS_ABI_VERSION 4
 #define WS_PAGE_SIZE 64
 
 typedef enum {
@@ -246,6 +246,47 @@ int ws_block_causal_attn_fwd_text(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_n
                                   float scale, int32_t flags,
                                   ws_tensor4 out, float *lse,
                                   void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * ws_block_causal_attn_fwd_varlen -- a streaming step over streams whose new
+ * blocks differ in length (concurrent streams, each at its own unit: blocks
+ * hold varying numbers of visual, audio and text tokens, Sec. 2.2 and
+ * Sec. 2.4), padded to a common new_len.  Same arguments and errors as
+ * ws_block_causal_attn_fwd_text, plus
+ *   new_lens_host / _dev: int32 [batch], same values on host and device:
+ *                stream b's new block is its first new_lens[b] tokens,
+ *                1 <= new_lens[b] <= new_len; tokens past it are padding.
+ *   text_starts_host / _dev: as for ws_block_causal_attn_fwd_text, or both
+ *                NULL for no segment.
+ * New token t of stream b sees cache tokens [0, cache_lens[b]) and new tokens
+ * [0, min(new_lens[b], max(text_starts[b], t + 1))): padding is never a key
+ * (never read, so its contents do not matter) and, with WS_FUSE_APPEND, never
+ * committed: only positions [cache_lens[b], cache_lens[b] + new_lens[b]) of
+ * the cache are written.  Padding rows get outputs by the same rule.
+ * A length outside [1, new_len] gives WS_ERR_SHAPE.  Workspace as for
+ * ws_block_causal_attn_fwd (with max_b cache_lens[b] + new_lens[b] keys).
+ */
+int ws_block_causal_attn_fwd_varlen(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new,
+                                    const ws_paged_kv *kv,
+                                    const int32_t *cache_lens_host, const int32_t *cache_lens_dev,
+                                    const int32_t *new_lens_host, const int32_t *new_lens_dev,
+                                    const int32_t *text_starts_host, const int32_t *text_starts_dev,
+                                    int32_t batch, int32_t new_len, int32_t num_q_heads,
+                                    float scale, int32_t flags,
+                                    ws_tensor4 out, float *lse,
+                                    void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * ws_kv_append_varlen -- ws_kv_append for blocks of different lengths: only
+ * tokens t < new_lens[b] of stream b are committed (new_lens_host / _dev:
+ * int32 [batch], same values, 0 <= new_lens[b] <= new_len).  Same arguments
+ * and errors as ws_kv_append; a length outside [0, new_len] gives
+ * WS_ERR_SHAPE.
+ */
+int ws_kv_append_varlen(const ws_paged_kv *kv, int32_t batch,
+                        const int32_t *cache_lens_host, const int32_t *cache_lens_dev,
+                        const int32_t *new_lens_host, const int32_t *new_lens_dev,
+                        int32_t new_len, ws_tensor4 k_new, ws_tensor4 v_new, void *stream);
 
 /*
  * ws_block_causal_prefill_text -- whole sequences whose blocks end in

@@ -6,11 +6,13 @@ kernels of csrc/.  PyTorch supplies device memory and the current stream.
 If the library is missing this module raises; there is no fallback.
 
 Entry points (same names as the C ABI, without the ``ws_`` prefix):
-  kv_append(cache, cache_lens, k_new, v_new)
-  block_causal_attn_fwd(q, k_new, v_new, cache, cache_lens, ..., text_starts=None)
+  kv_append(cache, cache_lens, k_new, v_new, new_lens=None)
+  block_causal_attn_fwd(q, k_new, v_new, cache, cache_lens, ..., text_starts=None,
+                        new_lens=None)
   block_causal_prefill(q, k, v, block_offsets, ..., text_starts=None)
 (with text_starts: the *_text entry points, blocks ending in a token-causal
-segment)
+segment; with new_lens: the *_varlen entry points, new blocks of different
+lengths padded to a common one)
   block_causal_prefill_bwd(q, k, v, o, dout, lse, block_offsets, ...)
   workspace_bytes(op, batch, num_q_heads, num_kv_heads, max_q, max_k)
 """
@@ -87,6 +89,12 @@ def library():
         lib.ws_block_causal_attn_fwd_text.argtypes = [
             Tensor4, Tensor4, Tensor4, ctypes.POINTER(PagedKVDesc), P, P, P, P, I32, I32, I32, F, I32,
             Tensor4, P, P, ctypes.c_size_t, P]
+        lib.ws_block_causal_attn_fwd_varlen.restype = ctypes.c_int
+        lib.ws_block_causal_attn_fwd_varlen.argtypes = [
+            Tensor4, Tensor4, Tensor4, ctypes.POINTER(PagedKVDesc), P, P, P, P, P, P, I32, I32, I32, F, I32,
+            Tensor4, P, P, ctypes.c_size_t, P]
+        lib.ws_kv_append_varlen.restype = ctypes.c_int
+        lib.ws_kv_append_varlen.argtypes = [ctypes.POINTER(PagedKVDesc), I32, P, P, P, P, I32, Tensor4, Tensor4, P]
         lib.ws_block_causal_prefill_text.restype = ctypes.c_int
         lib.ws_block_causal_prefill_text.argtypes = [
             Tensor4, Tensor4, Tensor4, ctypes.POINTER(PagedKVDesc), P, P, P, P, I32, I32, I32, I32, I32,
@@ -95,7 +103,7 @@ def library():
         lib.ws_block_causal_prefill_bwd.argtypes = [
             Tensor4, Tensor4, Tensor4, Tensor4, Tensor4, P, P, P, P, P, I32, I32, I32, I32, I32, I32, F,
             Tensor4, Tensor4, Tensor4, P, ctypes.c_size_t, P]
-        if lib.ws_abi_version() != 3:
+        if lib.ws_abi_version() != 4:
             raise RuntimeError("libwsattn.so ABI version mismatch")
         _LIB = lib
     return _LIB
@@ -199,8 +207,9 @@ def workspace_bytes(op, batch, num_q_heads, num_kv_heads, max_q, max_k):
     return library().ws_workspace_bytes(op, batch, num_q_heads, num_kv_heads, max_q, max_k)
 
 
-def kv_append(cache, cache_lens, k_new, v_new):
-    """Commit k_new/v_new [B][Ln][Hkv][d] at positions cache_lens[b] + t."""
+def kv_append(cache, cache_lens, k_new, v_new, new_lens=None):
+    """Commit k_new/v_new [B][Ln][Hkv][d] at positions cache_lens[b] + t
+    (only t < new_lens[b] when new_lens, [B], is given)."""
     host, dev = _lens(cache_lens, k_new.device)
     B, Ln = k_new.shape[0], k_new.shape[1]
     _shape("k_new", k_new, (B, Ln, cache.num_kv_heads, cache.head_dim))
@@ -208,8 +217,14 @@ def kv_append(cache, cache_lens, k_new, v_new):
     _check_lens(host, dev, B)
     _check_table(cache, B)
     desc = cache.desc()
-    _check(library().ws_kv_append(ctypes.byref(desc), k_new.shape[0], host.data_ptr(), dev.data_ptr(),
-                                  k_new.shape[1], _t4(k_new), _t4(v_new), _stream()))
+    if new_lens is None:
+        _check(library().ws_kv_append(ctypes.byref(desc), B, host.data_ptr(), dev.data_ptr(),
+                                      Ln, _t4(k_new), _t4(v_new), _stream()))
+    else:
+        nh, nd = _int32_pair(new_lens, (B,), k_new.device)
+        _check(library().ws_kv_append_varlen(ctypes.byref(desc), B, host.data_ptr(), dev.data_ptr(),
+                                             nh.data_ptr(), nd.data_ptr(), Ln, _t4(k_new), _t4(v_new),
+                                             _stream()))
 
 
 def _int32_pair(x, shape, device):
@@ -229,12 +244,14 @@ def _int32_pair(x, shape, device):
 
 def block_causal_attn_fwd(q, k_new, v_new, cache, cache_lens, scale=None, fuse_append=False,
                           out=None, out_dtype=torch.bfloat16, want_lse=False, lse=None,
-                          workspace=None, text_starts=None):
+                          workspace=None, text_starts=None, new_lens=None):
     """One streaming step: q [B][Lq][Hq][d] of the new block attends to
     cache tokens [0, cache_lens[b]) and to its own block (k_new/v_new).
     text_starts (optional, [B]): the new block ends in a token-causal segment
     starting at that token of the block; new token t then sees new tokens
     [0, max(text_starts[b], t + 1)).
+    new_lens (optional, [B], 1..Lq): stream b's block is its first
+    new_lens[b] tokens; the rest is padding, never a key and never committed.
     Returns out (and lse [B][Hq][Lq] f32 when want_lse)."""
     B, Lq, Hq, D = q.shape
     host, dev = _lens(cache_lens, q.device)
@@ -252,7 +269,11 @@ def block_causal_attn_fwd(q, k_new, v_new, cache, cache_lens, scale=None, fuse_a
         raise ValueError("q head_dim differs from the cache's")
     _check_lens(host, dev, B)
     _check_table(cache, B)
-    max_k = int(host.max().item()) + Lq if B > 0 else Lq
+    nl = None if new_lens is None else _int32_pair(new_lens, (B,), q.device)
+    if nl is None or B == 0:
+        max_k = int(host.max().item()) + Lq if B > 0 else Lq
+    else:
+        max_k = max(int((host.to(torch.int64) + nl[0]).max().item()), Lq)
     need = workspace_bytes(WS_OP_STEP, B, Hq, cache.num_kv_heads, Lq, max_k) if B > 0 and Lq > 0 else 0
     if workspace is None and need > 0:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
@@ -260,7 +281,13 @@ def block_causal_attn_fwd(q, k_new, v_new, cache, cache_lens, scale=None, fuse_a
     ws_len = workspace.numel() if workspace is not None else 0
     desc = cache.desc()
     flags = WS_FUSE_APPEND if fuse_append else 0
-    if text_starts is None:
+    if nl is not None:
+        th, td = _int32_pair(text_starts, (B,), q.device) if text_starts is not None else (None, None)
+        _check(library().ws_block_causal_attn_fwd_varlen(
+            _t4(q), _t4(k_new), _t4(v_new), ctypes.byref(desc), host.data_ptr(), dev.data_ptr(),
+            nl[0].data_ptr(), nl[1].data_ptr(), _ptr(th), _ptr(td), B, Lq, Hq, float(scale), flags,
+            _t4(out), _ptr(lse), ws_ptr, ws_len, _stream()))
+    elif text_starts is None:
         _check(library().ws_block_causal_attn_fwd(
             _t4(q), _t4(k_new), _t4(v_new), ctypes.byref(desc), host.data_ptr(), dev.data_ptr(),
             B, Lq, Hq, float(scale), flags, _t4(out), _ptr(lse), ws_ptr, ws_len, _stream()))

@@ -175,10 +175,14 @@ bool finish_work(ws::AttnArgs &a) {
 
 int step_impl(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_kv *kv,
               const int32_t *cache_lens_host, const int32_t *cache_lens_dev,
+              const int32_t *nl_host, const int32_t *nl_dev,
               const int32_t *text_host, const int32_t *text_dev, int32_t batch,
               int32_t new_len, int32_t num_q_heads, float scale, int32_t flags,
               ws_tensor4 out, float *lse, void *workspace, size_t workspace_bytes,
               void *stream);
+int append_impl(const ws_paged_kv *kv, int32_t batch, const int32_t *cache_lens_host,
+                const int32_t *cache_lens_dev, const int32_t *nl_host, const int32_t *nl_dev, int32_t new_len,
+                ws_tensor4 k_new, ws_tensor4 v_new, void *stream);
 int prefill_impl(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, const ws_paged_kv *kv_or_null,
                  const int32_t *block_offsets_host, const int32_t *block_offsets_dev,
                  const int32_t *text_host, const int32_t *text_dev,
@@ -230,29 +234,15 @@ size_t ws_workspace_bytes(int32_t op, int32_t batch, int32_t num_q_heads, int32_
 int ws_kv_append(const ws_paged_kv *kv, int32_t batch, const int32_t *cache_lens_host,
                  const int32_t *cache_lens_dev, int32_t new_len, ws_tensor4 k_new, ws_tensor4 v_new,
                  void *stream) {
-    if (int rc = check_paged(kv)) return rc;
-    if (!cache_lens_host || !cache_lens_dev) return fail(WS_ERR_NULL, "cache_lens pointer is NULL");
-    if (batch < 0 || new_len < 0) return fail(WS_ERR_SHAPE, "batch %d, new_len %d", (int)batch, (int)new_len);
-    if (batch == 0 || new_len == 0) return ok();  // nothing is read or written
-    if (int rc = check_tensor("k_new", k_new, false)) return rc;
-    if (int rc = check_tensor("v_new", v_new, false)) return rc;
-    for (int b = 0; b < batch; ++b) {
-        if (cache_lens_host[b] < 0) return fail(WS_ERR_SHAPE, "cache_lens[%d] = %d", b, (int)cache_lens_host[b]);
-        if (int rc = check_pages(kv, b, (int64_t)cache_lens_host[b] + new_len)) return rc;
-    }
-    ws::AppendArgs a{};
-    a.kn = (const uint16_t *)k_new.ptr;
-    a.vn = (const uint16_t *)v_new.ptr;
-    a.kn_sb = k_new.stride_b; a.kn_st = k_new.stride_t; a.kn_sh = k_new.stride_h;
-    a.vn_sb = v_new.stride_b; a.vn_st = v_new.stride_t; a.vn_sh = v_new.stride_h;
-    a.kpool = (uint16_t *)kv->k_pool;
-    a.vpool = (uint16_t *)kv->v_pool;
-    a.page_table = kv->page_table_dev;
-    a.max_pages = kv->max_pages_per_seq;
-    a.cache_lens = cache_lens_dev;
-    a.B = batch; a.Ln = new_len; a.Hkv = kv->num_kv_heads; a.D = kv->head_dim;
-    if (int e = ws::launch_append(a, stream)) return fail(WS_ERR_HIP, "append launch failed (hip error %d)", e);
-    return ok();
+    return append_impl(kv, batch, cache_lens_host, cache_lens_dev, nullptr, nullptr, new_len, k_new, v_new, stream);
+}
+
+int ws_kv_append_varlen(const ws_paged_kv *kv, int32_t batch, const int32_t *cache_lens_host,
+                        const int32_t *cache_lens_dev, const int32_t *new_lens_host, const int32_t *new_lens_dev,
+                        int32_t new_len, ws_tensor4 k_new, ws_tensor4 v_new, void *stream) {
+    if (!new_lens_host || !new_lens_dev) return fail(WS_ERR_NULL, "new_lens pointer is NULL");
+    return append_impl(kv, batch, cache_lens_host, cache_lens_dev, new_lens_host, new_lens_dev, new_len, k_new,
+                       v_new, stream);
 }
 
 int ws_block_causal_attn_fwd(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_kv *kv,
@@ -260,8 +250,8 @@ int ws_block_causal_attn_fwd(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, c
                              int32_t new_len, int32_t num_q_heads, float scale, int32_t flags,
                              ws_tensor4 out, float *lse, void *workspace, size_t workspace_bytes,
                              void *stream) {
-    return step_impl(q, k_new, v_new, kv, cache_lens_host, cache_lens_dev, nullptr, nullptr, batch, new_len,
-                     num_q_heads, scale, flags, out, lse, workspace, workspace_bytes, stream);
+    return step_impl(q, k_new, v_new, kv, cache_lens_host, cache_lens_dev, nullptr, nullptr, nullptr, nullptr, batch,
+                     new_len, num_q_heads, scale, flags, out, lse, workspace, workspace_bytes, stream);
 }
 
 int ws_block_causal_attn_fwd_text(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_kv *kv,
@@ -271,8 +261,23 @@ int ws_block_causal_attn_fwd_text(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_n
                                   ws_tensor4 out, float *lse, void *workspace, size_t workspace_bytes,
                                   void *stream) {
     if (!text_starts_host || !text_starts_dev) return fail(WS_ERR_NULL, "text_starts pointer is NULL");
-    return step_impl(q, k_new, v_new, kv, cache_lens_host, cache_lens_dev, text_starts_host, text_starts_dev,
-                     batch, new_len, num_q_heads, scale, flags, out, lse, workspace, workspace_bytes, stream);
+    return step_impl(q, k_new, v_new, kv, cache_lens_host, cache_lens_dev, nullptr, nullptr, text_starts_host,
+                     text_starts_dev, batch, new_len, num_q_heads, scale, flags, out, lse, workspace,
+                     workspace_bytes, stream);
+}
+
+int ws_block_causal_attn_fwd_varlen(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_kv *kv,
+                                    const int32_t *cache_lens_host, const int32_t *cache_lens_dev,
+                                    const int32_t *new_lens_host, const int32_t *new_lens_dev,
+                                    const int32_t *text_starts_host, const int32_t *text_starts_dev,
+                                    int32_t batch, int32_t new_len, int32_t num_q_heads, float scale,
+                                    int32_t flags, ws_tensor4 out, float *lse, void *workspace,
+                                    size_t workspace_bytes, void *stream) {
+    if (!new_lens_host || !new_lens_dev) return fail(WS_ERR_NULL, "new_lens pointer is NULL");
+    if (!text_starts_host != !text_starts_dev) return fail(WS_ERR_NULL, "text_starts: give both copies or neither");
+    return step_impl(q, k_new, v_new, kv, cache_lens_host, cache_lens_dev, new_lens_host, new_lens_dev,
+                     text_starts_host, text_starts_dev, batch, new_len, num_q_heads, scale, flags, out, lse,
+                     workspace, workspace_bytes, stream);
 }
 
 int ws_block_causal_prefill(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, const ws_paged_kv *kv_or_null,
@@ -376,9 +381,43 @@ int ws_block_causal_prefill_bwd(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, ws_ten
 
 namespace {
 
-// One streaming step (text_* NULL: no token-causal segment).
+// Commit new tokens to the cache (nl_* NULL: new_len tokens per stream).
+int append_impl(const ws_paged_kv *kv, int32_t batch, const int32_t *cache_lens_host,
+                const int32_t *cache_lens_dev, const int32_t *nl_host, const int32_t *nl_dev, int32_t new_len,
+                ws_tensor4 k_new, ws_tensor4 v_new, void *stream) {
+    if (int rc = check_paged(kv)) return rc;
+    if (!cache_lens_host || !cache_lens_dev) return fail(WS_ERR_NULL, "cache_lens pointer is NULL");
+    if (batch < 0 || new_len < 0) return fail(WS_ERR_SHAPE, "batch %d, new_len %d", (int)batch, (int)new_len);
+    if (batch == 0 || new_len == 0) return ok();  // nothing is read or written
+    if (int rc = check_tensor("k_new", k_new, false)) return rc;
+    if (int rc = check_tensor("v_new", v_new, false)) return rc;
+    for (int b = 0; b < batch; ++b) {
+        if (cache_lens_host[b] < 0) return fail(WS_ERR_SHAPE, "cache_lens[%d] = %d", b, (int)cache_lens_host[b]);
+        if (nl_host && (nl_host[b] < 0 || nl_host[b] > new_len))
+            return fail(WS_ERR_SHAPE, "new_lens[%d] = %d outside [0, new_len %d]", b, (int)nl_host[b], (int)new_len);
+        if (int rc = check_pages(kv, b, (int64_t)cache_lens_host[b] + (nl_host ? nl_host[b] : new_len))) return rc;
+    }
+    ws::AppendArgs a{};
+    a.kn = (const uint16_t *)k_new.ptr;
+    a.vn = (const uint16_t *)v_new.ptr;
+    a.kn_sb = k_new.stride_b; a.kn_st = k_new.stride_t; a.kn_sh = k_new.stride_h;
+    a.vn_sb = v_new.stride_b; a.vn_st = v_new.stride_t; a.vn_sh = v_new.stride_h;
+    a.kpool = (uint16_t *)kv->k_pool;
+    a.vpool = (uint16_t *)kv->v_pool;
+    a.page_table = kv->page_table_dev;
+    a.max_pages = kv->max_pages_per_seq;
+    a.cache_lens = cache_lens_dev;
+    a.new_lens = nl_host ? nl_dev : nullptr;
+    a.B = batch; a.Ln = new_len; a.Hkv = kv->num_kv_heads; a.D = kv->head_dim;
+    if (int e = ws::launch_append(a, stream)) return fail(WS_ERR_HIP, "append launch failed (hip error %d)", e);
+    return ok();
+}
+
+// One streaming step (text_* NULL: no token-causal segment; nl_* NULL:
+// every new block holds new_len tokens).
 int step_impl(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_kv *kv,
               const int32_t *cache_lens_host, const int32_t *cache_lens_dev,
+              const int32_t *nl_host, const int32_t *nl_dev,
               const int32_t *text_host, const int32_t *text_dev, int32_t batch,
               int32_t new_len, int32_t num_q_heads, float scale, int32_t flags,
               ws_tensor4 out, float *lse, void *workspace, size_t workspace_bytes,
@@ -402,9 +441,12 @@ int step_impl(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_k
     int64_t max_k = 0;
     for (int b = 0; b < batch; ++b) {
         if (cache_lens_host[b] < 0) return fail(WS_ERR_SHAPE, "cache_lens[%d] = %d", b, (int)cache_lens_host[b]);
-        const int64_t need = (int64_t)cache_lens_host[b] + (fuse ? new_len : 0);
+        if (nl_host && (nl_host[b] < 1 || nl_host[b] > new_len))
+            return fail(WS_ERR_SHAPE, "new_lens[%d] = %d outside [1, new_len %d]", b, (int)nl_host[b], (int)new_len);
+        const int64_t nl = nl_host ? nl_host[b] : new_len;
+        const int64_t need = (int64_t)cache_lens_host[b] + (fuse ? nl : 0);
         if (int rc = check_pages(kv, b, need)) return rc;
-        if ((int64_t)cache_lens_host[b] + new_len > max_k) max_k = (int64_t)cache_lens_host[b] + new_len;
+        if ((int64_t)cache_lens_host[b] + nl > max_k) max_k = (int64_t)cache_lens_host[b] + nl;
     }
     if (max_k > INT32_MAX) return fail(WS_ERR_SHAPE, "too many keys");
     if (text_host)
@@ -447,11 +489,16 @@ int step_impl(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_k
         a.text_starts = text_dev;
         a.has_text = 1;
     }
+    if (nl_host) {
+        a.new_lens = nl_dev;
+        a.has_new_lens = 1;
+    }
     if (batch <= ws::LENS_IN_ARGS) {
         a.lens_in_args = 1;
         for (int b = 0; b < batch; ++b) {
             a.lens_arg[b] = cache_lens_host[b];
             a.text_arg[b] = text_host ? text_host[b] : new_len;
+            a.nl_arg[b] = nl_host ? nl_host[b] : new_len;
         }
     }
     if (!finish_work(a)) return fail(WS_ERR_SHAPE, "too many work items");

@@ -55,6 +55,11 @@ struct AttnArgs {
     // keys j < max(start, i + 1) (prefill positions; step: n_pool + that).
     const int32_t *text_starts;
     int32_t has_text;
+    // step: tokens of each stream's new block [B] (has_new_lens; else Lq).
+    // New token t sees n_pool + min(new_len_b, max(start, t + 1)) keys;
+    // tokens past new_len_b are padding: never keys, never committed.
+    const int32_t *new_lens;
+    int32_t has_new_lens;
     // output [B][Lq][Hq][D] (bf16 or f32) and lse [B][Hq][Lq] (nullable)
     void *out;
     int64_t o_sb, o_st, o_sh;
@@ -94,6 +99,7 @@ struct AttnArgs {
     int32_t lens_in_args;
     int32_t lens_arg[32];
     int32_t text_arg[32];   // step: segment starts by value (new_len: none)
+    int32_t nl_arg[32];     // step: new-block lengths by value
 };
 
 constexpr int LENS_IN_ARGS = 32;
@@ -106,6 +112,7 @@ struct AppendArgs {
     const int32_t *page_table;
     int32_t max_pages;
     const int32_t *cache_lens;
+    const int32_t *new_lens;   // NULL: every stream commits Ln tokens
     int32_t B, Ln, Hkv, D;
 };
 

@@ -253,15 +253,17 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     // give the keys all rows see (kfull) and the keys any row sees (k_hi).
     const int32_t *offs = step ? nullptr : a.offsets + (int64_t)b * (a.nb + 1);
     const int32_t *text = (!step && a.has_text) ? a.text_starts + (int64_t)b * a.nb : nullptr;
-    int n_pool, k_hi, kfull, ts = 0;
+    int n_pool, k_hi, kfull, ts = 0, nl = 0;
     if (step) {
         n_pool = !a.lens_in_args ? ld_uniform(a.cache_lens, b) : b == 0 ? (int)lens0 : a.lens_arg[b];
-        // start of the new block's token-causal segment (Lq: none); new
-        // token t sees n_pool + max(ts, t + 1) keys
+        // start of the new block's token-causal segment (Lq: none) and the
+        // block's length (Lq: no padding); new token t sees
+        // n_pool + min(nl, max(ts, t + 1)) keys
         ts = a.lens_in_args ? a.text_arg[b] : a.has_text ? ld_uniform(a.text_starts, b) : a.Lq;
+        nl = a.lens_in_args ? a.nl_arg[b] : a.has_new_lens ? ld_uniform(a.new_lens, b) : a.Lq;
         const int t_last = (int)fastdiv((uint32_t)(min(q0 + QT, (int)nrows) - 1), fd_gq);
-        k_hi = n_pool + max(ts, t_last + 1);
-        kfull = n_pool + max(ts, (int)fastdiv((uint32_t)q0, fd_gq) + 1);
+        k_hi = n_pool + min(nl, max(ts, t_last + 1));
+        kfull = n_pool + min(nl, max(ts, (int)fastdiv((uint32_t)q0, fd_gq) + 1));
     } else {
         n_pool = a.paged ? a.Lq : 0;
         const int q_last = min(q0 + QT, a.Lq) - 1;
@@ -297,7 +299,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
         const int pc = min(row[n], (int)nrows - 1);
         tok[n] = row_token(pc);
         hqr[n] = row_head(pc, tok[n]);
-        kend[n] = step ? n_pool + max(ts, tok[n] + 1) : row_key_end<false>(offs, text, a.nb, tok[n]);
+        kend[n] = step ? n_pool + min(nl, max(ts, tok[n] + 1)) : row_key_end<false>(offs, text, a.nb, tok[n]);
     }
 
     // ---- direct-to-LDS tile loads -----------------------------------------
@@ -763,7 +765,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     // ---- fused append -----------------------------------------------------
     // Step items cover every query head of their KV group (packed rows),
     // so the items of a (stream, KV head) group split the new tokens evenly
-    // among them.
+    // among them; padding tokens (t >= nl) are not committed.
     // This kernel reads the new block from kc/vc, never from the slots being
     // written, so the append can trail the attention; it comes after the
     // epilogue's stores so that its loads overlap their drain.
@@ -772,7 +774,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
         const int napp = a.nqt * a.nsplit;
         const int ai = qi * a.nsplit + split;
         const int s0 = (int)((int64_t)ai * a.Lq / napp);
-        const int n = ((int)((int64_t)(ai + 1) * a.Lq / napp) - s0) * CH;
+        const int n = max(min((int)((int64_t)(ai + 1) * a.Lq / napp), nl) - s0, 0) * CH;
         for (int u = tid; u < n; u += NT) {
             const int t = s0 + u / CH, c = u % CH;
             const int pos = n_pool + t;
@@ -920,8 +922,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const AttnArgs a) {
 // contiguous 256-byte runs (head_dim 128).
 __global__ __launch_bounds__(256) void append_kernel(const AppendArgs a) {
     const int CH = a.D / 8;
-    const int64_t total = (int64_t)a.Ln * a.Hkv * CH;
     const int b = blockIdx.y;
+    const int64_t total = (int64_t)(a.new_lens ? a.new_lens[b] : a.Ln) * a.Hkv * CH;
     for (int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x; u < total; u += (int64_t)gridDim.x * 256) {
         const int c = (int)(u % CH);
         const int h = (int)((u / CH) % a.Hkv);

@@ -109,6 +109,9 @@ class Workload:
     # token-causal segments: prefill [B][nb] absolute starts; step [B]
     # starts within the new block (None: plain block-causal)
     text_starts: Optional[np.ndarray] = None
+    # step: tokens of each stream's new block [B] (None: all Lq); the rest
+    # of the Lq positions is padding
+    new_lens: Optional[np.ndarray] = None
 
     # step views: the cache part and the new block of the logical K/V
     @property

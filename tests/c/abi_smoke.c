@@ -29,6 +29,9 @@ int main(void) {
     CHECK(ws_block_causal_attn_fwd(none, none, none, NULL, lens, lens, 1, 4, 2, 0.1f, 0, none, NULL,
                                    NULL, 0, NULL) == WS_ERR_NULL);
     CHECK(strlen(ws_last_error()) > 0);
+    CHECK(ws_block_causal_attn_fwd_varlen(none, none, none, NULL, lens, lens, lens, lens, NULL, NULL, 1, 4, 2,
+                                          0.1f, 0, none, NULL, NULL, 0, NULL) == WS_ERR_NULL);
+    CHECK(ws_kv_append_varlen(NULL, 1, lens, lens, NULL, NULL, 4, none, none, NULL) == WS_ERR_NULL);
     /* negative sizes */
     int32_t offs[2] = {0, 8};
     CHECK(ws_block_causal_prefill(none, none, none, NULL, offs, offs, -1, 8, 1, 2, 1, 64, 0.1f, none,

@@ -84,7 +84,8 @@ def run_gpu(wl, cache=None, out_dtype=None, want_lse=True, fuse=None):
     fuse = wl.fuse_append if fuse is None else fuse
     return ws.block_causal_attn_fwd(q, to_dev_bf16(wl.k_new), to_dev_bf16(wl.v_new), cache,
                                     wl.cache_lens, scale=wl.scale, fuse_append=fuse,
-                                    out_dtype=out_dtype, want_lse=want_lse, text_starts=wl.text_starts)
+                                    out_dtype=out_dtype, want_lse=want_lse, text_starts=wl.text_starts,
+                                    new_lens=wl.new_lens)
 
 
 def run_oracle(wl, rows=None):
@@ -94,7 +95,7 @@ def run_oracle(wl, rows=None):
                               wl.offsets, wl.scale, rows=rows, text_starts=wl.text_starts)
     return oracle.step(inputs.bf16_bits(wl.q), inputs.bf16_bits(wl.k_cache), inputs.bf16_bits(wl.v_cache),
                        wl.cache_lens, inputs.bf16_bits(wl.k_new), inputs.bf16_bits(wl.v_new), wl.scale,
-                       rows=rows, text_starts=wl.text_starts)
+                       rows=rows, text_starts=wl.text_starts, new_lens=wl.new_lens)
 
 
 def compare(out, lse, ref_out, ref_lse, rows=None):

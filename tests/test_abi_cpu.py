@@ -42,10 +42,11 @@ def test_exports_every_declared_symbol(lib):
     names = header_functions()
     assert {"ws_kv_append", "ws_block_causal_attn_fwd", "ws_block_causal_prefill",
             "ws_block_causal_attn_fwd_text", "ws_block_causal_prefill_text", "ws_block_causal_prefill_bwd",
+            "ws_block_causal_attn_fwd_varlen", "ws_kv_append_varlen",
             "ws_workspace_bytes", "ws_abi_version", "ws_status_string", "ws_last_error"} <= set(names)
     for name in names:
         assert hasattr(lib, name), name
-    assert lib.ws_abi_version() == 3
+    assert lib.ws_abi_version() == 4
     assert lib.ws_status_string(0) == b"WS_OK"
     assert lib.ws_status_string(10) == b"WS_ERR_HIP"
 
@@ -202,6 +203,63 @@ def test_step_text_errors(lib):
     assert step_text_call(lib, h, [-1, 3]) == 5
     # valid starts (0 and new_len) pass to the next check: a misaligned lse
     assert step_text_call(lib, h, [0, 16], lse=FAKE + 2) == 4
+
+
+def step_varlen_call(lib, h, new_lens, starts=None, B=2, Lq=16, Hq=4, flags=0, lse=None, wsb=1 << 30,
+                     nl_dev=FAKE, starts_dev=FAKE):
+    desc = h.desc()
+    nl = np.ascontiguousarray(np.asarray(new_lens, np.int32)) if new_lens is not None else None
+    st = np.ascontiguousarray(np.asarray(starts, np.int32)) if starts is not None else None
+    return lib.ws_block_causal_attn_fwd_varlen(
+        t4(H=Hq, L=Lq), t4(H=2, L=Lq), t4(H=2, L=Lq), ctypes.byref(desc), h.lens.ctypes.data, FAKE,
+        nl.ctypes.data if nl is not None else None, nl_dev,
+        st.ctypes.data if st is not None else None, starts_dev if st is not None else None,
+        B, Lq, Hq, 0.088, flags, t4(H=Hq, L=Lq), lse, FAKE, wsb, None)
+
+
+def test_step_varlen_errors(lib):
+    h = Host()
+    assert step_varlen_call(lib, h, None) == 1                  # NULL host lengths
+    assert step_varlen_call(lib, h, [16, 3], nl_dev=None) == 1
+    assert step_varlen_call(lib, h, [16, 0]) == 2               # an empty block
+    assert step_varlen_call(lib, h, [17, 3]) == 2               # longer than new_len
+    assert step_varlen_call(lib, h, [16, 3], starts=[0, 17]) == 5
+    # valid lengths (1 and new_len) pass to the next check: a misaligned lse
+    assert step_varlen_call(lib, h, [16, 1], starts=[0, 16], lse=FAKE + 2) == 4
+    assert step_varlen_call(lib, h, [16, 1], lse=FAKE + 2) == 4
+    # host starts without device starts
+    desc = h.desc()
+    nl = np.array([16, 3], np.int32)
+    st = np.array([0, 3], np.int32)
+    assert lib.ws_block_causal_attn_fwd_varlen(
+        t4(), t4(H=2), t4(H=2), ctypes.byref(desc), h.lens.ctypes.data, FAKE, nl.ctypes.data, FAKE,
+        st.ctypes.data, None, 2, 16, 4, 0.088, 0, t4(), None, FAKE, 1 << 30, None) == 1
+
+
+def test_step_varlen_capacity_counts_real_tokens(lib):
+    # 4 pages hold 256 tokens: stream 1 (250 cached) can commit 6 new tokens, not 7
+    h = Host(lens=(10, 250))
+    assert step_varlen_call(lib, h, [16, 7], flags=ws.WS_FUSE_APPEND) == 7
+    # 6 fits and reaches the workspace check (the 256-key range is split)
+    assert step_varlen_call(lib, h, [16, 6], flags=ws.WS_FUSE_APPEND, wsb=16) == 9
+
+
+def append_varlen_call(lib, h, new_lens, Ln=16, nl_dev=FAKE, kn=None):
+    desc = h.desc()
+    nl = np.ascontiguousarray(np.asarray(new_lens, np.int32)) if new_lens is not None else None
+    return lib.ws_kv_append_varlen(ctypes.byref(desc), 2, h.lens.ctypes.data, FAKE,
+                                   nl.ctypes.data if nl is not None else None, nl_dev, Ln,
+                                   kn or t4(H=2, L=Ln), t4(H=2, L=Ln), None)
+
+
+def test_append_varlen_errors(lib):
+    h = Host(lens=(10, 250))
+    assert append_varlen_call(lib, h, None) == 1
+    assert append_varlen_call(lib, h, [1, 2], nl_dev=None) == 1
+    assert append_varlen_call(lib, h, [-1, 2]) == 2
+    assert append_varlen_call(lib, h, [17, 2]) == 2
+    assert append_varlen_call(lib, h, [16, 7]) == 7              # 250 + 7 > 256
+    assert append_varlen_call(lib, h, [16, 6], kn=t4(ptr=FAKE + 8)) == 4
 
 
 def prefill_text_call(lib, offs, starts, B=1, starts_dev=FAKE, lse=None):
