@@ -58,13 +58,15 @@ def kernel_source_hash():
 def visible_pairs(wl):
     """Visible (query, key) pairs per (stream, query head).  With token-causal
     segments (text_starts), token i of a block with segment start ts sees
-    max(ts, i + 1) keys (step: after the stream's cache)."""
+    max(ts, i + 1) keys (step: after the stream's cache).  Steps over padded
+    blocks (new_lens) count the real tokens only."""
     ts_all = getattr(wl, "text_starts", None)
     if wl.kind == "step":
         out = []
         for b, c in enumerate(wl.cache_lens):
-            lq = int(wl.Lq)
-            ts = lq if ts_all is None else int(ts_all[b])
+            nls = getattr(wl, "new_lens", None)
+            lq = int(wl.Lq) if nls is None else int(nls[b])
+            ts = lq if ts_all is None else min(int(ts_all[b]), lq)
             # sum over t < lq of max(ts, t + 1)
             own = ts * ts + (lq * (lq + 1) - ts * (ts + 1)) // 2
             out.append(lq * int(c) + own)
@@ -91,12 +93,17 @@ def algorithmic_bytes(wl):
     block's writes when it is committed."""
     e = 2  # bf16
     out_e = 4 if wl.out_f32 else 2
+    if wl.kind == "step":
+        # real tokens only when the blocks are padded
+        nls = getattr(wl, "new_lens", None)
+        n_new = [int(wl.Lq)] * wl.B if nls is None else [int(n) for n in nls]
+        q = sum(n_new) * wl.Hq * wl.D * e
+        o = sum(n_new) * wl.Hq * wl.D * out_e
+        kv = 2 * sum(int(c) + n for c, n in zip(wl.cache_lens, n_new)) * wl.Hkv * wl.D * e
+        app = 2 * sum(n_new) * wl.Hkv * wl.D * e if wl.fuse_append else 0
+        return q + kv + o + app
     q = wl.B * wl.Lq * wl.Hq * wl.D * e
     o = wl.B * wl.Lq * wl.Hq * wl.D * out_e
-    if wl.kind == "step":
-        kv = 2 * sum(int(c) + wl.Lq for c in wl.cache_lens) * wl.Hkv * wl.D * e
-        app = 2 * wl.B * wl.Lq * wl.Hkv * wl.D * e if wl.fuse_append else 0
-        return q + kv + o + app
     kv = 2 * wl.B * wl.Lq * wl.Hkv * wl.D * e
     return q + kv + o
 
@@ -125,6 +132,10 @@ class DeviceCase:
             if wl.text_starts is not None:
                 th = torch.from_numpy(np.ascontiguousarray(wl.text_starts, dtype=np.int32))
                 self.text = (th, th.to(dev))
+            self.new_lens = None
+            if wl.new_lens is not None:
+                nh = torch.from_numpy(np.ascontiguousarray(wl.new_lens, dtype=np.int32))
+                self.new_lens = (nh, nh.to(dev))
             kc = wl.k_cache.contiguous().to(dev)
             vc = wl.v_cache.contiguous().to(dev)
             n = int(wl.cache_lens.min())
@@ -132,8 +143,11 @@ class DeviceCase:
             zero = torch.zeros(wl.B, dtype=torch.int32)
             ws.kv_append(self.cache, (zero, zero.to(dev)), kc[:, :n], vc[:, :n])
             del kc, vc
-            need = ws.workspace_bytes(ws.WS_OP_STEP, wl.B, wl.Hq, wl.Hkv, wl.Lq,
-                                      int(wl.cache_lens.max()) + wl.Lq)
+            if wl.new_lens is None:
+                need = ws.workspace_bytes(ws.WS_OP_STEP, wl.B, wl.Hq, wl.Hkv, wl.Lq,
+                                          int(wl.cache_lens.max()) + wl.Lq)
+            else:
+                need = ws.step_workspace_bytes_varlen(wl.B, wl.Hq, wl.Hkv, wl.Lq, wl.cache_lens, wl.new_lens)
             self.workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
         else:
             off = torch.from_numpy(wl.offsets.astype(np.int32))
@@ -161,7 +175,7 @@ class DeviceCase:
             ws.block_causal_attn_fwd(self.q, self.k_new, self.v_new, self.cache, self.lens,
                                      scale=wl.scale, fuse_append=wl.fuse_append, out=self.out,
                                      lse=self.lse, want_lse=True, workspace=self.workspace,
-                                     text_starts=self.text)
+                                     text_starts=self.text, new_lens=self.new_lens)
         else:
             ws.block_causal_prefill(self.q, self.k, self.v, self.offsets, scale=wl.scale,
                                     cache=self.cache, num_kv_heads=wl.Hkv, out=self.out,
@@ -517,12 +531,14 @@ def main():
 
     extra = []
     if not args.no_extra:
-        for idx in (3, 4, 5, "thinker"):
+        for idx in (3, 4, 5, "thinker", "varlen"):
             if idx == args.config:
                 continue
             # "thinker": the interleaved workload with each unit's text
-            # segment token-causal
-            w2 = inputs.thinker_prefill() if idx == "thinker" else inputs.config(idx)
+            # segment token-causal; "varlen": four streams each ingesting an
+            # interleaved unit of its own length in one step
+            w2 = (inputs.thinker_prefill() if idx == "thinker" else inputs.streams_varlen() if idx == "varlen"
+                  else inputs.config(idx))
             f2, b2 = algorithmic_flops(w2), algorithmic_bytes(w2)
             wms, emean, emed, _ = time_workload(w2, max(3, args.steps // 5), 2, dev, latency_steps=0)
             extra.append({"workload": w2.name, "ms": round(emean, 4), "TFLOP/s": round(f2 / (emean * 1e-3) / 1e12, 1),

@@ -262,9 +262,13 @@ int ws_block_causal_attn_fwd_text(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_n
  * [0, min(new_lens[b], max(text_starts[b], t + 1))): padding is never a key
  * (never read, so its contents do not matter) and, with WS_FUSE_APPEND, never
  * committed: only positions [cache_lens[b], cache_lens[b] + new_lens[b]) of
- * the cache are written.  Padding rows get outputs by the same rule.
- * A length outside [1, new_len] gives WS_ERR_SHAPE.  Workspace as for
- * ws_block_causal_attn_fwd (with max_b cache_lens[b] + new_lens[b] keys).
+ * the cache are written.  The outputs and lse of padding rows are
+ * unspecified: query tiles holding padding only are skipped (no work, no
+ * store), so a short block costs about its own length, not new_len.
+ * A length outside [1, new_len] gives WS_ERR_SHAPE.  workspace: at least
+ * ws_step_workspace_bytes_varlen(batch, num_q_heads, kv->num_kv_heads,
+ * new_len, cache_lens_host, new_lens_host) bytes (the KV split count
+ * depends on the lengths, so ws_workspace_bytes does not give it).
  */
 int ws_block_causal_attn_fwd_varlen(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new,
                                     const ws_paged_kv *kv,
@@ -275,6 +279,16 @@ int ws_block_causal_attn_fwd_varlen(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v
                                     float scale, int32_t flags,
                                     ws_tensor4 out, float *lse,
                                     void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * ws_step_workspace_bytes_varlen -- device workspace bytes that
+ * ws_block_causal_attn_fwd_varlen needs for these host arrays (int32
+ * [batch] each; the same WS_SPLITS setting applies).  0 when none is needed
+ * or when an argument is invalid (the call itself then reports why).
+ */
+size_t ws_step_workspace_bytes_varlen(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                      int32_t new_len, const int32_t *cache_lens_host,
+                                      const int32_t *new_lens_host);
 
 /*
  * ws_kv_append_varlen -- ws_kv_append for blocks of different lengths: only

@@ -15,6 +15,7 @@ segment; with new_lens: the *_varlen entry points, new blocks of different
 lengths padded to a common one)
   block_causal_prefill_bwd(q, k, v, o, dout, lse, block_offsets, ...)
   workspace_bytes(op, batch, num_q_heads, num_kv_heads, max_q, max_k)
+  step_workspace_bytes_varlen(batch, num_q_heads, num_kv_heads, new_len, cache_lens, new_lens)
 """
 import ctypes
 import math
@@ -25,7 +26,8 @@ import torch  # loads the HIP runtime that libwsattn.so then shares
 from . import build as _build
 
 __all__ = ["WsError", "PagedCache", "kv_append", "block_causal_attn_fwd",
-           "block_causal_prefill", "block_causal_prefill_bwd", "workspace_bytes", "library",
+           "block_causal_prefill", "block_causal_prefill_bwd", "workspace_bytes",
+           "step_workspace_bytes_varlen", "library",
            "abi_version", "WS_OP_STEP", "WS_OP_PREFILL", "WS_OP_PREFILL_BWD", "PAGE_SIZE"]
 
 WS_DTYPE_BF16, WS_DTYPE_F32 = 1, 2
@@ -93,6 +95,8 @@ def library():
         lib.ws_block_causal_attn_fwd_varlen.argtypes = [
             Tensor4, Tensor4, Tensor4, ctypes.POINTER(PagedKVDesc), P, P, P, P, P, P, I32, I32, I32, F, I32,
             Tensor4, P, P, ctypes.c_size_t, P]
+        lib.ws_step_workspace_bytes_varlen.restype = ctypes.c_size_t
+        lib.ws_step_workspace_bytes_varlen.argtypes = [I32, I32, I32, I32, P, P]
         lib.ws_kv_append_varlen.restype = ctypes.c_int
         lib.ws_kv_append_varlen.argtypes = [ctypes.POINTER(PagedKVDesc), I32, P, P, P, P, I32, Tensor4, Tensor4, P]
         lib.ws_block_causal_prefill_text.restype = ctypes.c_int
@@ -207,6 +211,15 @@ def workspace_bytes(op, batch, num_q_heads, num_kv_heads, max_q, max_k):
     return library().ws_workspace_bytes(op, batch, num_q_heads, num_kv_heads, max_q, max_k)
 
 
+def step_workspace_bytes_varlen(batch, num_q_heads, num_kv_heads, new_len, cache_lens, new_lens):
+    """Workspace bytes of a step over blocks of different lengths (host
+    int32 arrays or tensors of [batch])."""
+    ch = torch.as_tensor(cache_lens, dtype=torch.int32).cpu().contiguous()
+    nh = torch.as_tensor(new_lens, dtype=torch.int32).cpu().contiguous()
+    return library().ws_step_workspace_bytes_varlen(batch, num_q_heads, num_kv_heads, new_len, ch.data_ptr(),
+                                                    nh.data_ptr())
+
+
 def kv_append(cache, cache_lens, k_new, v_new, new_lens=None):
     """Commit k_new/v_new [B][Ln][Hkv][d] at positions cache_lens[b] + t
     (only t < new_lens[b] when new_lens, [B], is given)."""
@@ -251,7 +264,8 @@ def block_causal_attn_fwd(q, k_new, v_new, cache, cache_lens, scale=None, fuse_a
     starting at that token of the block; new token t then sees new tokens
     [0, max(text_starts[b], t + 1)).
     new_lens (optional, [B], 1..Lq): stream b's block is its first
-    new_lens[b] tokens; the rest is padding, never a key and never committed.
+    new_lens[b] tokens; the rest is padding, never a key and never committed,
+    and its rows' out and lse are unspecified.
     Returns out (and lse [B][Hq][Lq] f32 when want_lse)."""
     B, Lq, Hq, D = q.shape
     host, dev = _lens(cache_lens, q.device)
@@ -270,11 +284,12 @@ def block_causal_attn_fwd(q, k_new, v_new, cache, cache_lens, scale=None, fuse_a
     _check_lens(host, dev, B)
     _check_table(cache, B)
     nl = None if new_lens is None else _int32_pair(new_lens, (B,), q.device)
-    if nl is None or B == 0:
-        max_k = int(host.max().item()) + Lq if B > 0 else Lq
+    if B == 0 or Lq == 0:
+        need = 0
+    elif nl is None:
+        need = workspace_bytes(WS_OP_STEP, B, Hq, cache.num_kv_heads, Lq, int(host.max().item()) + Lq)
     else:
-        max_k = max(int((host.to(torch.int64) + nl[0]).max().item()), Lq)
-    need = workspace_bytes(WS_OP_STEP, B, Hq, cache.num_kv_heads, Lq, max_k) if B > 0 and Lq > 0 else 0
+        need = step_workspace_bytes_varlen(B, Hq, cache.num_kv_heads, Lq, host, nl[0])
     if workspace is None and need > 0:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
     ws_ptr = _ptr(workspace)

@@ -3,11 +3,13 @@
 // Plain C++ (no HIP headers): every argument is checked here before any
 // device work is enqueued, so a rejected call leaves all device memory
 // untouched.  Kernels are reached through the launchers of ws_kernels.hip.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <vector>
 
 #include "../../include/ws_attn.h"
 #include "ws_kernels.h"
@@ -109,29 +111,75 @@ struct StepPlan {
     int nsplit;
 };
 
-// Query tile and KV split count of a streaming step.  Splits are added only
-// while the work-groups still fit one round on the CUs, and every split
-// keeps at least two 64-key tiles.
+// Query tile and KV split count of a streaming step.
 // One launch shape: 8 waves x 32 query rows (256-query tiles).
 ws::TileShape default_shape() { return ws::TileShape{1, 8}; }
 
+// Per-item fixed cost (prologue, epilogue, partial stores) in units of one
+// 64-key tile of the loop, for the split model below.
+constexpr int64_t SPLIT_FIXED_TILES = 4;
+
 // The step packs the G query heads of a KV group into one row space of
-// G * lq rows (see AttnArgs).
-StepPlan plan_step(int batch, int hq, int hkv, int lq, int64_t max_k) {
+// G * lq rows (see AttnArgs).  Split count: by default the largest that
+// still fits the work-groups in one round on the CUs (every split keeps at
+// least two 64-key tiles).  A round-count model, rounds(s) x (tiles per
+// split + fixed cost), replaces it when it predicts a gain of more than 10 %:
+// when the items do not fill the last round (a batch of 3 or 5 long
+// streams, or new blocks of different lengths, nl != NULL, whose tiles of
+// padding only do no work).
+StepPlan plan_step(int batch, int hq, int hkv, int lq, int64_t max_k, const int32_t *nl = nullptr) {
     StepPlan p;
     p.shape = default_shape();
     const int64_t qt = p.shape.qtile();
-    const int64_t rows = (int64_t)(hq / hkv) * lq;
-    p.nqt = (int)((rows + qt - 1) / qt);
-    const int64_t base = (int64_t)batch * hkv * p.nqt;
+    const int64_t G = hq / hkv;
+    p.nqt = (int)((G * lq + qt - 1) / qt);
+    // work items with at least one real row, per split
+    int64_t base = (int64_t)batch * hkv * p.nqt;
+    if (nl) {
+        base = 0;
+        for (int b = 0; b < batch; ++b) base += (G * nl[b] + qt - 1) / qt;
+        base *= hkv;
+    }
     const int64_t ntiles = (max_k + 63) / 64;
     const int64_t slots = (int64_t)NUM_CUS * p.shape.groups_per_cu();
-    int64_t ns = 1;
-    // the largest split count that still fits one round of work-groups
-    if (base > 0 && base < slots) ns = slots / base;
-    if (ns > ntiles / 2) ns = ntiles / 2;
-    if (ns > WS_MAX_SPLITS) ns = WS_MAX_SPLITS;
-    if (ns < 1) ns = 1;
+    int64_t cap = ntiles / 2;
+    if (cap > WS_MAX_SPLITS) cap = WS_MAX_SPLITS;
+    if (cap < 1) cap = 1;
+    int64_t ns = (base > 0 && base < slots) ? slots / base : 1;
+    if (ns > cap) ns = cap;
+    // real q-tiles of the streams before stream b (nl only)
+    std::vector<int64_t> pre(nl ? batch + 1 : 0);
+    if (nl)
+        for (int b = 0; b < batch; ++b) pre[b + 1] = pre[b] + (G * nl[b] + qt - 1) / qt;
+    // rounds of work-groups x (tiles per split + fixed cost)
+    auto cost = [&](int64_t s) -> int64_t {
+        const int64_t per_split = (ntiles + s - 1) / s + SPLIT_FIXED_TILES;
+        if (!nl) return (base * s + slots - 1) / slots * per_split;
+        // Items of padding only finish at once, so rounds are counted per
+        // XCD, from the real items in its range of the launch order: groups
+        // KV-head-major (g = kvh * batch + b), P = nqt * s items per group,
+        // of which the first (real tiles of b) * s are real.
+        const int64_t P = (int64_t)p.nqt * s, n_work = (int64_t)batch * hkv * P;
+        const int64_t per = (n_work + ws::NUM_XCD - 1) / ws::NUM_XCD;
+        auto real_before = [&](int64_t w) -> int64_t {   // real items in [0, w)
+            if (w >= n_work) return hkv * pre[batch] * s;
+            const int64_t g = w / P, kvh = g / batch, b = g % batch;
+            return (kvh * pre[batch] + pre[b]) * s + std::min(w - g * P, (pre[b + 1] - pre[b]) * s);
+        };
+        const int64_t per_cu = slots / ws::NUM_XCD;
+        int64_t rounds = 0;
+        for (int64_t x = 0; x < ws::NUM_XCD; ++x) {
+            const int64_t c = real_before((x + 1) * per) - real_before(x * per);
+            rounds = std::max(rounds, (c + per_cu - 1) / per_cu);
+        }
+        return rounds * per_split;
+    };
+    if (base > 0) {
+        int64_t best = 1;
+        for (int64_t s = 2; s <= cap; ++s)
+            if (cost(s) < cost(best)) best = s;
+        if (10 * cost(best) < 9 * cost(ns)) ns = best;
+    }
     const int s_env = env_int("WS_SPLITS", 0);
     if (s_env > 0) ns = s_env > WS_MAX_SPLITS ? WS_MAX_SPLITS : s_env;
     p.nsplit = (int)ns;
@@ -161,7 +209,7 @@ bool finish_work(ws::AttnArgs &a) {
     const int64_t n = (int64_t)a.B * a.Hkv * a.gi * a.nqt * a.nsplit;
     if (n > (int64_t)1 << 30) return false;
     a.n_work = (int32_t)n;
-    a.per_xcd = (a.n_work + 7) / 8;
+    a.per_xcd = (a.n_work + ws::NUM_XCD - 1) / ws::NUM_XCD;
     a.per_qt = a.gi * a.nsplit;
     a.per_group = a.per_qt * a.nqt;
     a.fd_group = ws::fastdiv_make((uint32_t)a.per_group);
@@ -170,6 +218,7 @@ bool finish_work(ws::AttnArgs &a) {
     a.fd_gq = ws::fastdiv_make((uint32_t)a.G);
     a.fd_hkv = ws::fastdiv_make((uint32_t)a.Hkv);
     a.fd_split = ws::fastdiv_make((uint32_t)a.nsplit);
+    a.fd_b = ws::fastdiv_make((uint32_t)a.B);
     return true;
 }
 
@@ -229,6 +278,23 @@ size_t ws_workspace_bytes(int32_t op, int32_t batch, int32_t num_q_heads, int32_
     if ((int64_t)(num_q_heads / num_kv_heads) * max_q > WS_MAX_STEP_ROWS) return 0;
     const StepPlan p = plan_step(batch, num_q_heads, num_kv_heads, max_q, max_k);
     return step_workspace(p, batch, num_q_heads, num_kv_heads, max_q);
+}
+
+size_t ws_step_workspace_bytes_varlen(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t new_len,
+                                      const int32_t *cache_lens_host, const int32_t *new_lens_host) {
+    if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads || new_len <= 0 ||
+        !cache_lens_host || !new_lens_host)
+        return 0;
+    if ((int64_t)(num_q_heads / num_kv_heads) * new_len > WS_MAX_STEP_ROWS) return 0;
+    int64_t max_k = 0;
+    for (int b = 0; b < batch; ++b) {
+        if (cache_lens_host[b] < 0 || new_lens_host[b] < 1 || new_lens_host[b] > new_len) return 0;
+        const int64_t k = (int64_t)cache_lens_host[b] + new_lens_host[b];
+        if (k > max_k) max_k = k;
+    }
+    if (max_k > INT32_MAX) return 0;
+    const StepPlan p = plan_step(batch, num_q_heads, num_kv_heads, new_len, max_k, new_lens_host);
+    return step_workspace(p, batch, num_q_heads, num_kv_heads, new_len);
 }
 
 int ws_kv_append(const ws_paged_kv *kv, int32_t batch, const int32_t *cache_lens_host,
@@ -456,7 +522,7 @@ int step_impl(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_k
                             (int)new_len);
     if ((int64_t)(num_q_heads / kv->num_kv_heads) * new_len > WS_MAX_STEP_ROWS)
         return fail(WS_ERR_SHAPE, "new_len x query heads per KV head exceeds %lld", (long long)WS_MAX_STEP_ROWS);
-    const StepPlan plan = plan_step(batch, num_q_heads, kv->num_kv_heads, new_len, max_k);
+    const StepPlan plan = plan_step(batch, num_q_heads, kv->num_kv_heads, new_len, max_k, nl_host);
     const size_t need_ws = step_workspace(plan, batch, num_q_heads, kv->num_kv_heads, new_len);
     if (need_ws > 0 && (!workspace || workspace_bytes < need_ws || !aligned16(workspace)))
         return fail(WS_ERR_WORKSPACE, "workspace needs %zu bytes (16-byte aligned), got %zu", need_ws,

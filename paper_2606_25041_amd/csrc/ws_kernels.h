@@ -9,6 +9,10 @@ namespace ws {
 enum { MODE_PREFILL = 0, MODE_STEP = 1 };
 
 constexpr int MAX_SPLITS = 32;   // KV splits of one step at most
+// MI355X: 8 XCDs; work-groups are dispatched to them round-robin, and the
+// attention kernel gives XCD x the contiguous work items
+// [x * per_xcd, (x + 1) * per_xcd)
+constexpr int NUM_XCD = 8;
 
 // Division by a divisor d (1 <= d < 2^31) fixed for a launch, exact for
 // dividends n < 2^31: with l = ceil(log2 d), mul = ceil(2^(31+l) / d) and
@@ -57,7 +61,8 @@ struct AttnArgs {
     int32_t has_text;
     // step: tokens of each stream's new block [B] (has_new_lens; else Lq).
     // New token t sees n_pool + min(new_len_b, max(start, t + 1)) keys;
-    // tokens past new_len_b are padding: never keys, never committed.
+    // tokens past new_len_b are padding: never keys, never committed, and
+    // tiles (and combine rows) of padding only are skipped.
     const int32_t *new_lens;
     int32_t has_new_lens;
     // output [B][Lq][Hq][D] (bf16 or f32) and lse [B][Hq][Lq] (nullable)
@@ -92,6 +97,7 @@ struct AttnArgs {
     // dividers by per_group, per_qt, G, Hkv and nsplit
     FastDiv fd_group, fd_qt, fd_g, fd_hkv, fd_split;
     FastDiv fd_gq;       // divider by G (packed row -> token)
+    FastDiv fd_b;        // divider by B (step groups taken KV-head-major)
     float scale_log2;    // scale * log2(e)
     // step: cache lengths (and segment starts) also passed by value when
     // batch <= LENS_IN_ARGS, so the first page lookup does not wait on a load

@@ -53,7 +53,6 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int KT = 64;        // keys per tile (= page size)
-constexpr int NUM_XCD = 8;    // MI355X: 8 XCDs, work-groups dispatched round-robin
 constexpr float RESCALE_LOG2 = 8.f;  // lazy-rescale threshold (log2 units)
 constexpr int PAGE_LDS = 2560;       // page ids of a split staged in LDS (more: read from memory)
 constexpr int NSTAGE = 4;            // K/V tiles resident in the LDS ring
@@ -162,6 +161,25 @@ __device__ __forceinline__ void dma16s(const char *base, uint32_t off, uint32_t 
 }
 #pragma clang diagnostic pop
 
+// The fused append's share of step work item ai (of nqt * nsplit per
+// (stream, KV head)): the group's items split the new tokens evenly; tokens
+// t >= nl are padding and not committed.  One 16-byte chunk per thread.
+template <int D, int NT>
+__device__ __forceinline__ void append_share(const AttnArgs &a, int b, int kvh, int ai, int n_pool, int nl,
+                                             const int32_t *ptab, int tid) {
+    constexpr int CH = D / 8;
+    const int napp = a.nqt * a.nsplit;
+    const int s0 = (int)((int64_t)ai * a.Lq / napp);
+    const int n = max(min((int)((int64_t)(ai + 1) * a.Lq / napp), nl) - s0, 0) * CH;
+    for (int u = tid; u < n; u += NT) {
+        const int t = s0 + u / CH, c = u % CH;
+        const int pos = n_pool + t;
+        const int64_t dst = (((int64_t)ptab[pos >> 6] * a.Hkv + kvh) * KT + (pos & 63)) * D + 8 * c;
+        *(u32x4 *)(a.kpool + dst) = *(const u32x4 *)(a.kc + b * a.kc_sb + (int64_t)t * a.kc_st + kvh * a.kc_sh + 8 * c);
+        *(u32x4 *)(a.vpool + dst) = *(const u32x4 *)(a.vc + b * a.vc_sb + (int64_t)t * a.vc_st + kvh * a.vc_sh + 8 * c);
+    }
+}
+
 template <int D, int NW, int NB>
 __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     constexpr int NT = NW * 64;
@@ -187,6 +205,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     const uint32_t bid = blockIdx.x;
     uint32_t per_xcd = a.per_xcd, n_work = a.n_work, per_group = a.per_group, per_qt = a.per_qt;
     uint32_t G = a.G, gi = a.gi, Hkv = a.Hkv, mode = a.mode, nqt = a.nqt, nrows = a.nrows, lens0 = a.lens_arg[0];
+    uint32_t has_nl = a.has_new_lens;
     FastDiv fd_group = a.fd_group, fd_qt = a.fd_qt, fd_g = a.fd_g, fd_hkv = a.fd_hkv, fd_split = a.fd_split;
     FastDiv fd_gq = a.fd_gq;
     const uint16_t *qptr = a.q;
@@ -195,7 +214,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
                       "+s"(mode), "+s"(nqt), "+s"(nrows), "+s"(lens0), "+s"(fd_group.mul), "+s"(fd_group.shift),
                       "+s"(fd_qt.mul), "+s"(fd_qt.shift), "+s"(fd_g.mul), "+s"(fd_g.shift), "+s"(fd_hkv.mul),
                       "+s"(fd_hkv.shift), "+s"(fd_split.mul), "+s"(fd_split.shift), "+s"(fd_gq.mul),
-                      "+s"(fd_gq.shift), "+s"(qptr), "+s"(q_sb), "+s"(q_st), "+s"(q_sh));
+                      "+s"(fd_gq.shift), "+s"(qptr), "+s"(q_sb), "+s"(q_st), "+s"(q_sh), "+s"(has_nl));
     const uint32_t w = (bid % NUM_XCD) * per_xcd + bid / NUM_XCD;
     if (w >= n_work) return;
     const uint32_t group = fastdiv(w, fd_group);
@@ -204,8 +223,18 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     const uint32_t rem = idx - qi * per_qt;
     const uint32_t split = fastdiv(rem, fd_g);
     const int hh = (int)(rem - split * gi);
-    const int b = (int)fastdiv(group, fd_hkv);
-    const int kvh = (int)(group - b * Hkv);
+    // Groups are taken stream-major; a step over blocks of different lengths
+    // takes them KV-head-major instead, so that the contiguous range of items
+    // each XCD runs mixes long and short streams rather than holding a few
+    // streams only.
+    int b, kvh;
+    if (has_nl) {
+        kvh = (int)fastdiv(group, a.fd_b);
+        b = (int)(group - (uint32_t)kvh * (uint32_t)a.B);
+    } else {
+        b = (int)fastdiv(group, fd_hkv);
+        kvh = (int)(group - b * Hkv);
+    }
     const int hq = kvh * (int)G + hh;   // (prefill; a step's rows span the group's heads)
     const bool step = mode == MODE_STEP;
     // token and query head of packed row p (see AttnArgs)
@@ -223,6 +252,22 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     // issue no tile loads) take the first blocks, so a small block's rows go
     // to waves without load duty
     const int rblk = (wave + NW / 2) % NW;
+
+    // A step tile whose first token lies past its stream's new block (blocks
+    // of different lengths, padded) holds no real row: it computes nothing
+    // and leaves its rows' outputs unwritten, but still does its share of
+    // the fused append.  Decided before any load is issued.
+    if (step && has_nl) {
+        const int nl0 = a.lens_in_args ? a.nl_arg[b] : ld_uniform(a.new_lens, b);
+        if ((int)fastdiv((uint32_t)q0, fd_gq) >= nl0) {
+            if (a.fuse_append) {
+                const int np0 = a.lens_in_args ? a.lens_arg[b] : ld_uniform(a.cache_lens, b);
+                append_share<D, NT>(a, b, kvh, (int)(qi * a.nsplit + split), np0, nl0,
+                                    a.page_table + (int64_t)b * a.max_pages, tid);
+            }
+            return;
+        }
+    }
 
     // Query rows of this wave go global -> LDS -> registers, issued first
     // thing: the direct loads stay in order with the tile loads, so one
@@ -769,20 +814,8 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     // This kernel reads the new block from kc/vc, never from the slots being
     // written, so the append can trail the attention; it comes after the
     // epilogue's stores so that its loads overlap their drain.
-    if (step && a.fuse_append && hh == 0) {
-        constexpr int CH = D / 8;
-        const int napp = a.nqt * a.nsplit;
-        const int ai = qi * a.nsplit + split;
-        const int s0 = (int)((int64_t)ai * a.Lq / napp);
-        const int n = max(min((int)((int64_t)(ai + 1) * a.Lq / napp), nl) - s0, 0) * CH;
-        for (int u = tid; u < n; u += NT) {
-            const int t = s0 + u / CH, c = u % CH;
-            const int pos = n_pool + t;
-            const int64_t dst = (((int64_t)ptab[pos >> 6] * a.Hkv + kvh) * KT + (pos & 63)) * D + 8 * c;
-            *(u32x4 *)(a.kpool + dst) = *(const u32x4 *)(a.kc + b * a.kc_sb + (int64_t)t * a.kc_st + kvh * a.kc_sh + 8 * c);
-            *(u32x4 *)(a.vpool + dst) = *(const u32x4 *)(a.vc + b * a.vc_sb + (int64_t)t * a.vc_st + kvh * a.vc_sh + 8 * c);
-        }
-    }
+    if (step && a.fuse_append && hh == 0)
+        append_share<D, NT>(a, b, kvh, (int)(qi * a.nsplit + split), n_pool, nl, ptab, tid);
 }
 
 // bf16 output: split s holds o_s / l_s (bf16) and lse_s = m_s + log2(l_s);
@@ -805,6 +838,7 @@ __global__ __launch_bounds__(256) void combine16_kernel(const AttnArgs a) {
     const int kvh = (int)((blk / a.nrb) % a.Hkv);
     const int b = (int)(blk / ((int64_t)a.nrb * a.Hkv));
     const int t = r / a.G;
+    if (a.has_new_lens && t >= a.new_lens[b]) return;   // padding row: left unwritten
     const int hq = kvh * a.G + (r - t * a.G);
     const int S = a.nsplit;
     const float *pl = a.part_ml + blk * 32 + (lane & 31);
@@ -877,6 +911,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const AttnArgs a) {
     const int kvh = (int)((blk / a.nrb) % a.Hkv);
     const int b = (int)(blk / ((int64_t)a.nrb * a.Hkv));
     const int t = r / a.G;
+    if (a.has_new_lens && t >= a.new_lens[b]) return;   // padding row: left unwritten
     const int hq = kvh * a.G + (r - t * a.G);
     const int d0 = 32 * (mg >> 2) + 8 * (mg & 3) + 4 * (lane >> 5);
     const int S = a.nsplit;

@@ -213,6 +213,21 @@ def thinker_step(B=4, Hq=64, Hkv=8, Lq=8, Lc=131072, seed=1007):
     return wl
 
 
+def streams_varlen(B=4, Hq=64, Hkv=8, Lc=131072, seed=1008):
+    """B concurrent streams, each ingesting its next interleaved unit (token
+    counts from ``interleaved_segments``, the unit's text segment token-causal
+    at its end) in one step, padded to the longest unit, over Lc cached
+    tokens (GQA Hq/Hkv x 128), committed in the same launch."""
+    vis, aud, txt = interleaved_segments(rng(seed, S_LENGTHS), B)
+    lens = vis + aud + txt
+    Lq = int(lens.max())
+    wl = step_workload(f"streams_varlen_b{B}_gqa{Hq}x{Hkv}_d128_q{Lq}_c{Lc}", B, Hq, Hkv, 128, Lq, [Lc] * B,
+                       seed, fuse_append=True)
+    wl.new_lens = lens.astype(np.int32)
+    wl.text_starts = (vis + aud).astype(np.int32)
+    return wl
+
+
 def sample_rows(g, B, Hq, L, n, must=()):
     """n distinct (b, h, i) rows (plus the given ones) for sampled checks."""
     rows = {tuple(int(x) for x in r) for r in must}

@@ -42,7 +42,7 @@ def test_exports_every_declared_symbol(lib):
     names = header_functions()
     assert {"ws_kv_append", "ws_block_causal_attn_fwd", "ws_block_causal_prefill",
             "ws_block_causal_attn_fwd_text", "ws_block_causal_prefill_text", "ws_block_causal_prefill_bwd",
-            "ws_block_causal_attn_fwd_varlen", "ws_kv_append_varlen",
+            "ws_block_causal_attn_fwd_varlen", "ws_kv_append_varlen", "ws_step_workspace_bytes_varlen",
             "ws_workspace_bytes", "ws_abi_version", "ws_status_string", "ws_last_error"} <= set(names)
     for name in names:
         assert hasattr(lib, name), name
@@ -242,6 +242,31 @@ def test_step_varlen_capacity_counts_real_tokens(lib):
     assert step_varlen_call(lib, h, [16, 7], flags=ws.WS_FUSE_APPEND) == 7
     # 6 fits and reaches the workspace check (the 256-key range is split)
     assert step_varlen_call(lib, h, [16, 6], flags=ws.WS_FUSE_APPEND, wsb=16) == 9
+
+
+def test_step_workspace_bytes_varlen(lib):
+    def wsv(B, hq, hkv, lq, lens, nls):
+        ch = np.ascontiguousarray(np.asarray(lens, np.int32))
+        nh = np.ascontiguousarray(np.asarray(nls, np.int32))
+        return lib.ws_step_workspace_bytes_varlen(B, hq, hkv, lq, ch.ctypes.data, nh.ctypes.data)
+    lens = [131072] * 4
+    # equal lengths: the plain step's plan
+    for lq, c in ((512, 131072), (243, 131072), (8, 131072), (256, 4096)):
+        assert wsv(4, 64, 8, lq, [c] * 4, [lq] * 4) == lib.ws_workspace_bytes(ws.WS_OP_STEP, 4, 64, 8, lq, c + lq)
+    # four long streams padded to 243 tokens fill the CUs exactly (no split,
+    # no workspace); with their real lengths 72 of the 256 work-groups hold
+    # padding only, and the KV range is split instead
+    assert wsv(4, 64, 8, 243, lens, [243] * 4) == 0
+    assert wsv(4, 64, 8, 243, lens, [145, 110, 163, 243]) > 0
+    # a batch of 3 long 512-token blocks (384 work-groups: 1.5 rounds) splits too
+    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 3, 64, 8, 512, 131072 + 512) > 0
+    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 4, 64, 8, 512, 131072 + 512) == 0
+    # invalid arguments give 0
+    assert wsv(4, 64, 8, 243, lens, [145, 0, 163, 243]) == 0
+    assert wsv(4, 64, 8, 243, lens, [145, 244, 163, 243]) == 0
+    assert wsv(4, 64, 8, 243, [131072, -1, 5, 5], [145, 110, 163, 243]) == 0
+    assert wsv(4, 64, 7, 243, lens, [145, 110, 163, 243]) == 0
+    assert lib.ws_step_workspace_bytes_varlen(4, 64, 8, 243, None, None) == 0
 
 
 def append_varlen_call(lib, h, new_lens, Ln=16, nl_dev=FAKE, kn=None):

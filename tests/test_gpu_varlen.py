@@ -28,13 +28,29 @@ def _varlen(name, B, Hq, Hkv, D, Lq, lens, new_lens, seed, starts=None, fuse=Fal
     return wl
 
 
+def _real_rows(wl, heads=None):
+    """Every (b, h, t) with t a real token of stream b (padding rows'
+    outputs are unspecified)."""
+    heads = range(wl.Hq) if heads is None else heads
+    return np.array([(b, h, t) for b in range(wl.B) for h in heads for t in range(int(wl.new_lens[b]))],
+                    np.int32)
+
+
+def _real(out, lse, wl):
+    """The real rows' outputs and lse, flattened (for bitwise comparisons)."""
+    n = [int(x) for x in wl.new_lens]
+    return (torch.cat([out[b, :n[b]].reshape(-1) for b in range(wl.B)]),
+            torch.cat([lse[b, :, :n[b]].reshape(-1) for b in range(wl.B)]))
+
+
 def _check_full(wl, cache, **kw):
     gs.say(f"[gpu] {wl.name}: B={wl.B} Hq={wl.Hq} Hkv={wl.Hkv} D={wl.D} Lq={wl.Lq} "
            f"new_lens={wl.new_lens.tolist()[:8]} text={None if wl.text_starts is None else wl.text_starts.tolist()[:8]}")
     out, lse = gs.run_gpu(wl, cache=cache, **kw)
     torch.cuda.synchronize()
-    ref, ref_lse = gs.run_oracle(wl)
-    gs.assert_close(gs.compare(out, lse, ref, ref_lse))
+    rows = _real_rows(wl)
+    ref, ref_lse = gs.run_oracle(wl, rows=rows)
+    gs.assert_close(gs.compare(out, lse, ref, ref_lse, rows=rows))
     return out, lse
 
 
@@ -81,10 +97,13 @@ def test_step_varlen_many_streams_from_memory():
 
 
 def test_fused_append_commits_only_real_tokens():
-    """With WS_FUSE_APPEND the attention result is bitwise that of the plain
-    call, and the cache holds exactly the real tokens (padding slots keep
-    their NaN fill)."""
-    wl = _varlen("varlen_fused", 3, 8, 2, 128, 70, [10, 200, 640], [70, 1, 33], seed=77, starts=[70, 0, 5])
+    """With WS_FUSE_APPEND the attention result (real rows) is bitwise that
+    of the plain call, and the cache holds exactly the real tokens (padding
+    slots keep their NaN fill).  In streams 1 and 2 (1 and 50 of 70 tokens)
+    the second query tile (tokens 64..69) holds padding only and is skipped,
+    while its work items' share of the append (from token 35 on) still
+    holds real tokens of stream 2."""
+    wl = _varlen("varlen_fused", 3, 8, 2, 128, 70, [10, 200, 640], [70, 1, 50], seed=77, starts=[70, 0, 5])
     cache = gs.device_cache(wl, wl.cache_lens)
     a, la = gs.run_gpu(wl, cache=cache, fuse=False)
     torch.cuda.synchronize()
@@ -92,7 +111,9 @@ def test_fused_append_commits_only_real_tokens():
     gs.say("[gpu] varlen fused append")
     b, lb = gs.run_gpu(wl, cache=cache, fuse=True)
     torch.cuda.synchronize()
-    assert torch.equal(a, b) and torch.equal(la, lb)
+    ra, rla = _real(a, la, wl)
+    rb, rlb = _real(b, lb, wl)
+    assert torch.equal(ra, rb) and torch.equal(rla, rlb)
     ek, ev = _expected_pools(wl)
     assert np.array_equal(_pool_bits(cache.k_pool), ek)
     assert np.array_equal(_pool_bits(cache.v_pool), ev)
@@ -157,12 +178,12 @@ def test_thinker_decode_varlen_full_size():
         wl.k[b, wl.Lc_max + int(n):] = float("nan")
         wl.v[b, wl.Lc_max + int(n):] = float("nan")
     cache = gs.device_cache(wl, wl.cache_lens, fill_on_gpu=True)
-    rows = [(b, h, t) for b in range(wl.B) for h in (0, 9, 63) for t in range(wl.Lq)]
+    rows = _real_rows(wl, heads=(0, 9, 63))
     gs.say(f"[gpu] {wl.name} varlen {wl.new_lens.tolist()}: full size, {len(rows)} sampled rows")
     out, lse = gs.run_gpu(wl, cache=cache)
     torch.cuda.synchronize()
-    ref, ref_lse = gs.run_oracle(wl, rows=np.array(rows, np.int32))
-    gs.assert_close(gs.compare(out, lse, ref, ref_lse, rows=np.array(rows, np.int32)))
+    ref, ref_lse = gs.run_oracle(wl, rows=rows)
+    gs.assert_close(gs.compare(out, lse, ref, ref_lse, rows=rows))
     # committed slots: real tokens bit-exact, the slot after them untouched (NaN)
     kb = inputs.bf16_bits(wl.k_new)
     pk = cache.k_pool
@@ -175,3 +196,25 @@ def test_thinker_decode_varlen_full_size():
                 assert np.array_equal(got, kb[b, t]), (b, t)
             else:
                 assert np.all(got == gs.NAN_BITS), (b, t)
+
+
+def test_streams_varlen_full_size():
+    """The bench's mixed-unit workload at full size: 4 streams over 131072
+    cached tokens (GQA 64/8), each ingesting one interleaved unit of its own
+    length (text segment token-causal), padded to the longest; sampled rows
+    including each unit's first, segment-start and last token."""
+    wl = inputs.streams_varlen()
+    for b, n in enumerate(wl.new_lens):
+        wl.k[b, wl.Lc_max + int(n):] = float("nan")
+        wl.v[b, wl.Lc_max + int(n):] = float("nan")
+    cache = gs.device_cache(wl, wl.cache_lens, fill_on_gpu=True)
+    must = []
+    for b in range(wl.B):
+        n, ts = int(wl.new_lens[b]), int(wl.text_starts[b])
+        must += [(b, 0, 0), (b, 63, n - 1), (b, 17, ts), (b, 40, max(ts - 1, 0))]
+    rows = inputs.sample_rows(np.random.default_rng(9), wl.B, wl.Hq, int(wl.new_lens.min()), 40, must=must)
+    gs.say(f"[gpu] {wl.name} new_lens {wl.new_lens.tolist()}: full size, {len(rows)} sampled rows")
+    out, lse = gs.run_gpu(wl, cache=cache)
+    torch.cuda.synchronize()
+    ref, ref_lse = gs.run_oracle(wl, rows=rows)
+    gs.assert_close(gs.compare(out, lse, ref, ref_lse, rows=rows))
