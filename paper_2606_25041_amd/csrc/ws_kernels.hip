@@ -822,7 +822,9 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
 //   M = max_s lse_s,  L = sum_s 2^(lse_s - M),  o = sum_s 2^(lse_s - M) o_s / L.
 // A thread owns the 8 elements (two accumulator groups) one writer lane
 // stored with one 16-byte store, for every split.
-template <int D>
+// VARLEN: blocks of different lengths; padding rows are skipped (their
+// partials may not exist).
+template <int D, bool VARLEN>
 __global__ __launch_bounds__(256) void combine16_kernel(const AttnArgs a) {
     constexpr int MD = D / 32;
     constexpr int PER_BLK = 2 * MD * 64;      // 16-byte items per 32-row block
@@ -838,7 +840,7 @@ __global__ __launch_bounds__(256) void combine16_kernel(const AttnArgs a) {
     const int kvh = (int)((blk / a.nrb) % a.Hkv);
     const int b = (int)(blk / ((int64_t)a.nrb * a.Hkv));
     const int t = r / a.G;
-    if (a.has_new_lens && t >= a.new_lens[b]) return;   // padding row: left unwritten
+    if (VARLEN && t >= a.new_lens[b]) return;   // padding row: left unwritten
     const int hq = kvh * a.G + (r - t * a.G);
     const int S = a.nsplit;
     const float *pl = a.part_ml + blk * 32 + (lane & 31);
@@ -895,7 +897,7 @@ __global__ __launch_bounds__(256) void combine16_kernel(const AttnArgs a) {
 // thread owns the 4 elements one accumulator lane holds for one (md, g), so
 // its partial reads are the writer's contiguous 1 KB runs; the split loops
 // are unrolled so their independent loads are in flight together.
-template <int D>
+template <int D, bool VARLEN>
 __global__ __launch_bounds__(256) void combine_kernel(const AttnArgs a) {
     constexpr int MD = D / 32;
     constexpr int PER_BLK = MD * 4 * 64;      // float4 items per 32-row block
@@ -911,7 +913,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const AttnArgs a) {
     const int kvh = (int)((blk / a.nrb) % a.Hkv);
     const int b = (int)(blk / ((int64_t)a.nrb * a.Hkv));
     const int t = r / a.G;
-    if (a.has_new_lens && t >= a.new_lens[b]) return;   // padding row: left unwritten
+    if (VARLEN && t >= a.new_lens[b]) return;   // padding row: left unwritten
     const int hq = kvh * a.G + (r - t * a.G);
     const int d0 = 32 * (mg >> 2) + 8 * (mg & 3) + 4 * (lane >> 5);
     const int S = a.nsplit;
@@ -1407,21 +1409,21 @@ int launch_attention(const AttnArgs &a, int head_dim, TileShape shape, void *str
 
 int launch_combine(const AttnArgs &a, int head_dim, void *stream) {
     hipStream_t st = (hipStream_t)stream;
+    typedef void (*Kern)(const AttnArgs);
+    const bool vl = a.has_new_lens != 0;
     if (!a.out_f32) {
         const int64_t items = (int64_t)a.B * a.Hkv * a.nrb * (head_dim / 32) * 2 * 64;
         const int64_t grid = (items + 255) / 256;
-        if (head_dim == 128)
-            hipLaunchKernelGGL(combine16_kernel<128>, dim3((unsigned)grid), dim3(256), 0, st, a);
-        else
-            hipLaunchKernelGGL(combine16_kernel<64>, dim3((unsigned)grid), dim3(256), 0, st, a);
+        Kern k = head_dim == 128 ? (vl ? combine16_kernel<128, true> : combine16_kernel<128, false>)
+                                 : (vl ? combine16_kernel<64, true> : combine16_kernel<64, false>);
+        hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(256), 0, st, a);
         return (int)hipGetLastError();
     }
     const int64_t items = (int64_t)a.B * a.Hkv * a.nrb * (head_dim / 32) * 4 * 64;
     const int64_t grid = (items + 255) / 256;
-    if (head_dim == 128)
-        hipLaunchKernelGGL(combine_kernel<128>, dim3((unsigned)grid), dim3(256), 0, st, a);
-    else
-        hipLaunchKernelGGL(combine_kernel<64>, dim3((unsigned)grid), dim3(256), 0, st, a);
+    Kern k = head_dim == 128 ? (vl ? combine_kernel<128, true> : combine_kernel<128, false>)
+                             : (vl ? combine_kernel<64, true> : combine_kernel<64, false>);
+    hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(256), 0, st, a);
     return (int)hipGetLastError();
 }
 
