@@ -123,7 +123,8 @@ constexpr int64_t SPLIT_FIXED_TILES = 4;
 // G * lq rows (see AttnArgs).  Split count: by default the largest that
 // still fits the work-groups in one round on the CUs (every split keeps at
 // least two 64-key tiles).  A round-count model, rounds(s) x (tiles per
-// split + fixed cost), replaces it when it predicts a gain of more than 10 %:
+// split + fixed cost), minimised with a bias to fewer splits, replaces it
+// when it predicts a gain of more than 10 %:
 // when the items do not fill the last round (a batch of 3 or 5 long
 // streams, or new blocks of different lengths, nl != NULL, whose tiles of
 // padding only do no work).
@@ -175,9 +176,13 @@ StepPlan plan_step(int batch, int hq, int hkv, int lq, int64_t max_k, const int3
         return rounds * per_split;
     };
     if (base > 0) {
+        // the fewest splits within 2 % of the modelled minimum (each split
+        // adds merge work and thins the L2 reuse of a KV range across q-tiles,
+        // which the model leaves out)
+        int64_t lo = cost(1);
+        for (int64_t s = 2; s <= cap; ++s) lo = std::min(lo, cost(s));
         int64_t best = 1;
-        for (int64_t s = 2; s <= cap; ++s)
-            if (cost(s) < cost(best)) best = s;
+        while (50 * cost(best) > 51 * lo) ++best;
         if (10 * cost(best) < 9 * cost(ns)) ns = best;
     }
     const int s_env = env_int("WS_SPLITS", 0);

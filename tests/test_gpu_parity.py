@@ -167,3 +167,16 @@ def test_config5_streams_full_size():
         page = int(wl.page_table[b][pos // 64])
         got = cache.k_pool[page, :, pos % 64].cpu()
         assert torch.equal(got.view(torch.int16), kn[b, t].view(torch.int16))
+
+
+def test_long_streams_split_by_round_model_full_size():
+    """3 streams of 512-token blocks over 131072 cached tokens (GQA 64/8):
+    the 384 work-groups fill 1.5 rounds, so the planner splits the KV range
+    in two (workspace > 0); sampled rows of the first and last stream."""
+    B = 3
+    wl = inputs.step_workload(f"streams_b{B}_gqa64x8_d128_q512_c131072", B, 64, 8, 128, 512, [131072] * B,
+                              seed=1020 + B, fuse_append=True)
+    assert ws.workspace_bytes(ws.WS_OP_STEP, B, 64, 8, 512, 131072 + 512) > 0
+    cache = gs.device_cache(wl, wl.cache_lens, fill_on_gpu=True)
+    _sampled(wl, cache, must=[(0, 0, 0), (B - 1, 63, 511), (B - 1, 5, 100)], n=16)
+
