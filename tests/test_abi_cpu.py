@@ -358,3 +358,64 @@ def test_workspace_bytes(lib):
     assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 0, 24, 24, 256, 4352) == 0
     assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 1, 24, 5, 256, 4352) == 0   # 24 % 5 != 0
     assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 1, 24, 0, 256, 4352) == 0
+
+
+def _split_model(B, hq, hkv, lq, lens, nls):
+    """The documented split rule, written out by brute force: the default
+    (the largest split count whose work-groups fit one round of 256 CUs), and
+    rounds(s) x (ceil(tiles / s) + 4) counted per XCD over the real items of
+    the launch order (groups KV-head-major for blocks of different lengths),
+    the fewest splits within 2 % of its minimum taking over when that is
+    more than 10 % cheaper than the default.  Returns the split count."""
+    qt, slots, xcds, fixed = 256, 256, 8, 4
+    G = hq // hkv
+    nqt = -(-G * lq // qt)
+    real = [-(-G * n // qt) for n in nls] if nls is not None else [nqt] * B
+    base = hkv * sum(real)
+    ntiles = -(-max(c + (n if nls is not None else lq) for c, n in zip(lens, nls or [lq] * B)) // 64)
+    cap = max(1, min(ntiles // 2, 32))
+
+    def cost(s):
+        per_split = -(-ntiles // s) + fixed
+        if nls is None:
+            return -(-base * s // slots) * per_split
+        P = nqt * s
+        n_work = B * hkv * P
+        per = -(-n_work // xcds)
+        cnt = [0] * xcds
+        for g in range(B * hkv):
+            lo, hi = g * P, g * P + real[g % B] * s
+            for x in range(xcds):
+                cnt[x] += max(0, min(hi, (x + 1) * per) - max(lo, x * per))
+        return max(-(-c // (slots // xcds)) for c in cnt) * per_split
+
+    ns = min(slots // base if base < slots else 1, cap)
+    lo = min(cost(s) for s in range(1, cap + 1))
+    best = 1
+    while 50 * cost(best) > 51 * lo:
+        best += 1
+    return best if 10 * cost(best) < 9 * cost(ns) else ns
+
+
+def test_split_planner_matches_its_rule(lib):
+    """The library's split count (read back from the workspace size) equals
+    the rule computed by brute force, for equal and for different new-block
+    lengths, on random shapes."""
+    rng = np.random.default_rng(17)
+    for _ in range(150):
+        hkv = int(rng.choice([1, 2, 4, 8, 16]))
+        G = int(rng.choice([1, 2, 4, 8]))
+        B = int(rng.integers(1, 9))
+        lq = int(rng.integers(1, 600))
+        lens = [int(rng.choice([0, 100, 4096, 30000, 131072])) for _ in range(B)]
+        nls = [int(x) for x in rng.integers(1, lq + 1, size=B)]
+        rows = -(-G * lq // 32) * 32
+        unit = B * hkv * rows * 130 * 4
+        for var in (False, True):
+            if var:
+                ch, nh = np.array(lens, np.int32), np.array(nls, np.int32)
+                got = lib.ws_step_workspace_bytes_varlen(B, hkv * G, hkv, lq, ch.ctypes.data, nh.ctypes.data)
+            else:
+                got = lib.ws_workspace_bytes(ws.WS_OP_STEP, B, hkv * G, hkv, lq, max(lens) + lq)
+            ns = _split_model(B, hkv * G, hkv, lq, lens, nls if var else None)
+            assert got == (0 if ns == 1 else ns * unit), (B, hkv * G, hkv, lq, lens, nls, var, ns, got)
