@@ -30,6 +30,12 @@
  * j < max(tau, i + 1); tau = block end means no segment (plain
  * block-causal), tau = block start makes the block token-causal.
  *
+ * New blocks of different lengths (the *_varlen entry points).  Units hold
+ * varying numbers of visual, audio and text tokens (Sec. 2.2), so
+ * concurrent streams stepped in one launch carry new blocks of different
+ * lengths, padded to a common new_len.  Padding tokens are never keys and
+ * are never committed; the outputs of their rows are unspecified.
+ *
  * Conventions for every entry point
  * ---------------------------------
  * - Token tensors are 4-d [batch][tokens][heads][head_dim] described by
@@ -58,9 +64,10 @@
  *   allocation, no synchronisation, no memset), so a caller may record them
  *   into a HIP graph by stream capture, e.g. the performer's solver loop of a
  *   unit (Sec. 2.4).  A replay repeats the recorded call exactly: the host
- *   arrays (cache lengths, page ids, offsets, segment starts) are read when
- *   the call is recorded, and small batches pass cache lengths and segment
- *   starts to the kernels by value.
+ *   arrays (cache lengths, page ids, offsets, segment starts, new-block
+ *   lengths) are read when the call is recorded, and small batches pass
+ *   cache lengths, segment starts and new-block lengths to the kernels by
+ *   value.
  * - A call with no token to process (batch == 0, or new_len / seq_len == 0)
  *   returns WS_OK after checking its scalar arguments, enqueues nothing and
  *   accepts NULL tensor pointers.
