@@ -469,6 +469,8 @@ def main():
     ap.add_argument("--config", type=int, default=2, help="headline workload index (1-5)")
     ap.add_argument("--sweep-only", default=None, metavar="NAME",
                     help="only time the named KV-length sweep point(s), comma-separated (for profiling)")
+    ap.add_argument("--varlen-only", action="store_true",
+                    help="only time the four-stream step over units of different lengths (for profiling)")
     ap.add_argument("--bwd-only", action="store_true",
                     help="only time the gradients of the whole-sequence workload (for profiling)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -496,6 +498,13 @@ def main():
     ws.library()
     if args.bwd_only:
         print(json.dumps(backward_timing(dev, steps=args.steps)), flush=True)
+        return
+    if args.varlen_only:
+        w2 = inputs.streams_varlen()
+        f2, b2 = algorithmic_flops(w2), algorithmic_bytes(w2)
+        _, emean, _, _ = time_workload(w2, args.steps, args.warmup, dev, latency_steps=0)
+        print(json.dumps({"workload": w2.name, "new_lens": [int(x) for x in w2.new_lens], "ms": round(emean, 4),
+                          "TFLOP/s": round(f2 / (emean * 1e-3) / 1e12, 1), "flops": f2, "bytes": b2}), flush=True)
         return
     if args.sweep_only:
         names = set(args.sweep_only.split(","))
