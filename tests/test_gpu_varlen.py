@@ -218,3 +218,22 @@ def test_streams_varlen_full_size():
     torch.cuda.synchronize()
     ref, ref_lse = gs.run_oracle(wl, rows=rows)
     gs.assert_close(gs.compare(out, lse, ref, ref_lse, rows=rows))
+
+
+def test_many_streams_padding_tiles_fused_from_memory():
+    """40 streams (lengths and cache lengths read from device memory), GQA 8
+    (8 x 40 packed rows: two query tiles, the second starting at token 32),
+    d = 64, committed in the same launch: streams of at most 32 tokens skip
+    their second tile, whose work items still commit tokens from 20 on."""
+    g = np.random.default_rng(85)
+    lens = [int(x) for x in g.integers(0, 700, size=40)]
+    n_new = [int(x) for x in g.integers(1, 41, size=40)]
+    n_new[:4] = [21, 32, 33, 40]
+    wl = _varlen("varlen_b40_fused", 40, 8, 1, 64, 40, lens, n_new, seed=85, starts=g.integers(0, 41, size=40),
+                 fuse=True)
+    cache = gs.device_cache(wl, wl.cache_lens)
+    _check_full(wl, cache)
+    torch.cuda.synchronize()
+    ek, ev = _expected_pools(wl)
+    assert np.array_equal(_pool_bits(cache.k_pool), ek)
+    assert np.array_equal(_pool_bits(cache.v_pool), ev)
