@@ -823,9 +823,13 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
 // A thread owns the 8 elements (two accumulator groups) one writer lane
 // stored with one 16-byte store, for every split.
 // VARLEN: blocks of different lengths; padding rows are skipped (their
-// partials may not exist).
-template <int D, bool VARLEN>
+// partials may not exist).  SMAX >= nsplit: the split loops are unrolled
+// SMAX times (the launch takes the smallest of 8, 16, 32, which also keeps
+// the register count, and with it the waves per SIMD that hide the loads'
+// latency, down).
+template <int D, bool VARLEN, int SMAX>
 __global__ __launch_bounds__(256) void combine16_kernel(const AttnArgs a) {
+    static_assert(SMAX <= MAX_SPLITS, "at most MAX_SPLITS partials");
     constexpr int MD = D / 32;
     constexpr int PER_BLK = 2 * MD * 64;      // 16-byte items per 32-row block
     const int64_t nblk = (int64_t)a.B * a.Hkv * a.nrb;
@@ -848,10 +852,10 @@ __global__ __launch_bounds__(256) void combine16_kernel(const AttnArgs a) {
     const int64_t ls = nblk * 32;             // split stride of lse
     const int64_t ps = nblk * 32 * D;         // split stride of o
     // all loads first (one round trip), then the arithmetic
-    float lse[MAX_SPLITS];
-    u32x4 ov[MAX_SPLITS];
+    float lse[SMAX];
+    u32x4 ov[SMAX];
 #pragma unroll
-    for (int s = 0; s < MAX_SPLITS; ++s) {
+    for (int s = 0; s < SMAX; ++s) {
         if (s < S) {
             lse[s] = pl[s * ls];
             ov[s] = *(const u32x4 *)(po + s * ps);
@@ -862,12 +866,12 @@ __global__ __launch_bounds__(256) void combine16_kernel(const AttnArgs a) {
     }
     float M = -INFINITY;
 #pragma unroll
-    for (int s = 0; s < MAX_SPLITS; ++s) M = fmaxf(M, lse[s]);
+    for (int s = 0; s < SMAX; ++s) M = fmaxf(M, lse[s]);
     const float Mu = (M == -INFINITY) ? 0.f : M;
     float L = 0.f;
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int s = 0; s < MAX_SPLITS; ++s) {
+    for (int s = 0; s < SMAX; ++s) {
         const float wgt = __builtin_amdgcn_exp2f(lse[s] - Mu);   // 0 for absent splits
         L += wgt;
 #pragma unroll
@@ -1407,15 +1411,23 @@ int launch_attention(const AttnArgs &a, int head_dim, TileShape shape, void *str
     return (int)hipErrorInvalidValue;
 }
 
+typedef void (*CombineKern)(const AttnArgs);
+
+template <int D, bool VL>
+CombineKern combine16_for(int nsplit) {
+    return nsplit <= 8 ? combine16_kernel<D, VL, 8>
+         : nsplit <= 16 ? combine16_kernel<D, VL, 16> : combine16_kernel<D, VL, MAX_SPLITS>;
+}
+
 int launch_combine(const AttnArgs &a, int head_dim, void *stream) {
     hipStream_t st = (hipStream_t)stream;
-    typedef void (*Kern)(const AttnArgs);
+    typedef CombineKern Kern;
     const bool vl = a.has_new_lens != 0;
     if (!a.out_f32) {
         const int64_t items = (int64_t)a.B * a.Hkv * a.nrb * (head_dim / 32) * 2 * 64;
         const int64_t grid = (items + 255) / 256;
-        Kern k = head_dim == 128 ? (vl ? combine16_kernel<128, true> : combine16_kernel<128, false>)
-                                 : (vl ? combine16_kernel<64, true> : combine16_kernel<64, false>);
+        Kern k = head_dim == 128 ? (vl ? combine16_for<128, true>(a.nsplit) : combine16_for<128, false>(a.nsplit))
+                                 : (vl ? combine16_for<64, true>(a.nsplit) : combine16_for<64, false>(a.nsplit));
         hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(256), 0, st, a);
         return (int)hipGetLastError();
     }
