@@ -1,19 +1,27 @@
 """Benchmark of block-causal streaming attention on one MI355X.
 
-Headline workload: one streaming step of a 256-token block, MHA 24 x 128,
-against a 4096-token paged cache (64-token pages in seeded random order),
-with the block committed to the cache in the same launch (WS_FUSE_APPEND).
-A "step" is one ws_block_causal_attn_fwd call: plan/validate, append, K/V
-tile fetch, QK^T, online softmax, PV, split combine and epilogue.
+Headline workload (the largest single-GPU configuration): one streaming
+step of 4 concurrent streams, GQA 64 query / 8 KV heads x 128, each
+appending a 512-token block (committed in the same launch, WS_FUSE_APPEND)
+and attending to its own paged cache of 131072 tokens (64-token pages in
+seeded random order).  A "step" is one ws_block_causal_attn_fwd call:
+plan/validate, append, K/V tile fetch, QK^T, online softmax, PV, split
+merge (none here: the work items fill the chip) and epilogue.
 
 Timing: W warm-up steps, then K timed steps bracketed by
 torch.cuda.synchronize() (the wall clock gives `value`) and by two HIP events
 recorded on the stream the kernels run on (torch's current stream), which
-give the average step time used for the roofline.  Nothing else runs inside
-the timed region.  Afterwards a separate loop puts each step between two
-events for the per-block latency.  The inputs rotate over enough
-device-resident copies (> 512 MB in total) that no copy is still in the 256
-MB last-level cache when it is used again, so the step reads HBM.
+give the average kernel time per step used for the roofline.  Nothing else
+runs inside the timed region.  Afterwards a separate loop puts each step
+between two events for the per-block latency.  Inputs of small workloads
+rotate over enough device-resident copies (> 512 MB in total) that no copy
+is still in the 256 MB last-level cache when it is used again.
+
+Also reported: the single 256-token step over a 4096-token cache (its HBM
+roofline), the prefill workloads, KV-length sweeps, the streaming replay of
+the prefill workloads block by block, the practical MFMA and HBM-read
+ceilings measured in the same job, and the fp64 oracle timed on the host
+cores on a stated row sample of every workload.
 
 Prints one JSON line (see the metric/roofline/cpu_baseline fields).
 Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-extra]
@@ -428,19 +436,202 @@ def backward_timing(dev, steps=5):
     return out
 
 
-def cpu_baseline(wl):
-    """The fp64 oracle (as it stands) on the whole headline step."""
+def row_key_counts(wl, rows):
+    """Keys each sampled (b, h, i) row sees (block-causal, no segments): a
+    prefill row sees every token up to the end of its block, a step row its
+    stream's cache and the whole new block."""
+    rows = np.asarray(rows)
+    if wl.kind == "step":
+        return np.array([int(wl.cache_lens[b]) + wl.Lq for b in rows[:, 0]], dtype=np.int64)
+    out = np.empty(len(rows), dtype=np.int64)
+    for n, (b, _, i) in enumerate(rows):
+        off = wl.offsets[b]
+        out[n] = off[np.searchsorted(off, i, side="right")]
+    return out
+
+
+# pairs of (query, key) per oracle sample: ~5 s of fp64 work on 16 host cores
+ORACLE_PAIRS = 2.0e8
+
+
+def oracle_sample(wl, seed=11):
+    """The fp64 oracle (as it stands) on a bounded sample of a workload's
+    query rows: the whole workload when it has at most ORACLE_PAIRS visible
+    pairs, else distinct (stream, head, token) rows drawn uniformly from the
+    seed until the sample holds about that many.  Returns the timing record
+    (TFLOP/s of the sampled rows' algorithmic work)."""
     import oracle  # test infrastructure: only this baseline leg uses it
     threads = oracle.default_threads()
-    q, kc, vc = inputs.bf16_bits(wl.q), inputs.bf16_bits(wl.k_cache), inputs.bf16_bits(wl.v_cache)
-    kn, vn = inputs.bf16_bits(wl.k_new), inputs.bf16_bits(wl.v_new)
+    total_pairs = float(sum(visible_pairs(wl))) * wl.Hq
+    rows = None
+    if total_pairs > ORACLE_PAIRS:
+        per_row = total_pairs / (wl.B * wl.Hq * wl.Lq)
+        n = int(ORACLE_PAIRS / per_row)
+        rows = inputs.sample_rows(np.random.default_rng(seed), wl.B, wl.Hq, wl.Lq, n)
+        pairs = float(row_key_counts(wl, rows).sum())
+        sample = (f"{len(rows)} of {wl.B * wl.Hq * wl.Lq} query rows (stream, head, token) drawn "
+                  f"uniformly with seed {seed}, {pairs:.3g} visible pairs, fp64, {threads} threads")
+    else:
+        pairs = total_pairs
+        sample = f"the whole workload ({wl.B * wl.Hq * wl.Lq} query rows, {pairs:.3g} visible pairs), fp64, " \
+                 f"{threads} threads"
+    q = inputs.bf16_bits(wl.q)
     t0 = time.perf_counter()
-    oracle.step(q, kc, vc, wl.cache_lens, kn, vn, wl.scale, nthreads=threads)
+    if wl.kind == "step":
+        oracle.step(q, inputs.bf16_bits(wl.k_cache), inputs.bf16_bits(wl.v_cache), wl.cache_lens,
+                    inputs.bf16_bits(wl.k_new), inputs.bf16_bits(wl.v_new), wl.scale, rows=rows, nthreads=threads)
+    else:
+        oracle.prefill(q, inputs.bf16_bits(wl.k), inputs.bf16_bits(wl.v), wl.offsets, wl.scale, rows=rows,
+                       nthreads=threads)
     dt = time.perf_counter() - t0
-    return {"value": algorithmic_flops(wl) / dt / 1e12, "unit": "TFLOP/s", "cores": threads,
-            "kind": "oracle", "seconds": round(dt, 3),
-            "sample": f"the whole headline step ({wl.B * wl.Lq * wl.Hq} query rows x "
-                      f"{int(wl.cache_lens[0]) + wl.Lq} keys), fp64, {threads} threads"}
+    log(f"[bench] oracle {wl.name}: {dt:.2f} s for {pairs:.3g} pairs")
+    return {"workload": wl.name, "value": 4.0 * wl.D * pairs / dt / 1e12, "unit": "TFLOP/s", "cores": threads,
+            "kind": "oracle", "seconds": round(dt, 3), "sample": sample}
+
+
+def replay_timing(idx, dev, reps=5):
+    """Streaming replay (the prefill workloads run block by block): for block
+    j of every stream, one step whose cache is blocks < j (already committed)
+    and whose new block is block j, committed in the same launch.  The
+    cache sits in a paged pool (the workload's page table, or a seeded
+    random one for contiguous workloads).  Per-block latency = median over
+    ``reps`` replays of the events around each step; the whole pool is
+    reused by every step, as in the streaming loop (it fits the last-level
+    cache for these workloads)."""
+    wl = inputs.config(idx)
+    B, Hq, Hkv, D = wl.B, wl.Hq, wl.Hkv, wl.D
+    offs = wl.offsets
+    assert all(np.array_equal(offs[0], o) for o in offs), "streams share block offsets"
+    off = offs[0].astype(np.int64)
+    table, npages = wl.page_table, wl.num_pages
+    if table is None:
+        table, npages = inputs.page_table(inputs.rng(wl.seed, inputs.S_PAGES), B, max(1, -(-wl.Lq // 64)))
+    cache = ws.PagedCache.allocate(npages, Hkv, D, torch.from_numpy(table), device=dev, fill_bits=0x7FC1)
+    q, k, v = wl.q.to(dev), wl.k.to(dev), wl.v.to(dev)
+    odt = torch.float32 if wl.out_f32 else torch.bfloat16
+    steps, need = [], 16
+    for j in range(len(off) - 1):
+        s0, e0 = int(off[j]), int(off[j + 1])
+        if e0 == s0:
+            continue
+        lq = e0 - s0
+        lens = torch.full((B,), s0, dtype=torch.int32)
+        need = max(need, ws.workspace_bytes(ws.WS_OP_STEP, B, Hq, Hkv, lq, s0 + lq))
+        steps.append(dict(q=q[:, s0:e0], k=k[:, s0:e0], v=v[:, s0:e0], lens=(lens, lens.to(dev)),
+                          out=torch.empty((B, lq, Hq, D), dtype=odt, device=dev), c=s0, n=lq))
+    work = torch.empty(need, dtype=torch.uint8, device=dev)   # one workspace, reused by every step
+    for st in steps:
+        st["work"] = work
+
+    def run(st):
+        ws.block_causal_attn_fwd(st["q"], st["k"], st["v"], cache, st["lens"], scale=wl.scale,
+                                 fuse_append=True, out=st["out"], workspace=st["work"])
+
+    for st in steps:   # warm-up replay (also fills the cache)
+        run(st)
+    torch.cuda.synchronize()
+    ms = np.zeros((reps, len(steps)))
+    for r in range(reps):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in steps]
+        for (a, b), st in zip(ev, steps):
+            a.record()
+            run(st)
+            b.record()
+        torch.cuda.synchronize()
+        ms[r] = [a.elapsed_time(b) for a, b in ev]
+    med = np.median(ms, axis=0)
+    flops = 0.0
+    for st in steps:
+        flops += 4.0 * D * Hq * B * st["n"] * (st["c"] + st["n"])
+    total = float(med.sum())
+    log(f"[bench] replay {wl.name}: {len(steps)} blocks, {total:.3f} ms per replay "
+        f"({flops / (total * 1e-3) / 1e12:.0f} TFLOP/s)")
+    out = {"workload": f"replay_{wl.name}", "blocks": len(steps), "ms_per_replay": round(total, 4),
+           "TFLOP/s": round(flops / (total * 1e-3) / 1e12, 1),
+           "cache_tokens": [st["c"] for st in steps], "block_tokens": [st["n"] for st in steps],
+           "ms_per_block_median": [round(float(x), 4) for x in med],
+           "ms_per_block_p10": [round(float(x), 4) for x in np.percentile(ms, 10, axis=0)],
+           "ms_per_block_p90": [round(float(x), 4) for x in np.percentile(ms, 90, axis=0)]}
+    del cache, q, k, v, steps, work
+    torch.cuda.empty_cache()
+    return out
+
+
+def _ceil_lib():
+    import ctypes
+    lib = ctypes.CDLL(ws._build.CEIL_LIB)
+    lib.wsc_mfma_loop.restype = ctypes.c_int
+    lib.wsc_mfma_loop.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p]
+    lib.wsc_stream_read.restype = ctypes.c_int
+    lib.wsc_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int32,
+                                    ctypes.c_void_p]
+    return lib
+
+
+def ceilings(dev, reps=10):
+    """Practical ceilings measured in the same job (libwsceil.so): the dense
+    bf16 MFMA rate of 8-wave work-groups issuing register-operand MFMAs
+    (4 x 256 work-groups, 4 x 4096 MFMAs per wave), and the rate of reading
+    a 4 GiB buffer once with 16-byte non-temporal loads (8 work-groups of 256
+    threads per CU).  Median of ``reps`` event-timed launches each."""
+    lib = _ceil_lib()
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def timed(fn):
+        fn()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b in ev:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        return float(np.median([a.elapsed_time(b) for a, b in ev]))
+
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    ng, iters = 4 * cus, 4096
+    out = torch.empty(ng, dtype=torch.float32, device=dev)
+
+    def mf():
+        rc = lib.wsc_mfma_loop(out.data_ptr(), ng, iters, stream)
+        assert rc == 0, rc
+    ms = timed(mf)
+    mfma_tf = ng * 8 * iters * 4 * 32768 / (ms * 1e-3) / 1e12
+    nbytes = 4 << 30
+    buf = torch.empty(nbytes, dtype=torch.uint8, device=dev).fill_(3)
+    ng2 = 8 * cus
+    out2 = torch.empty(ng2, dtype=torch.int32, device=dev)
+
+    def rd():
+        rc = lib.wsc_stream_read(buf.data_ptr(), nbytes, out2.data_ptr(), ng2, stream)
+        assert rc == 0, rc
+    ms2 = timed(rd)
+    read_gbs = nbytes / (ms2 * 1e-3) / 1e9
+    log(f"[bench] ceilings: MFMA {mfma_tf:.0f} TFLOP/s, streaming read {read_gbs:.0f} GB/s")
+    del buf
+    torch.cuda.empty_cache()
+    return {"mfma_bf16_TFLOP/s": round(mfma_tf, 1), "mfma_frac_of_peak": round(mfma_tf / BF16_PEAK_TFLOPS, 4),
+            "hbm_read_GB/s": round(read_gbs, 1), "hbm_read_frac_of_peak": round(read_gbs / HBM_PEAK_GBS, 4),
+            "mfma_kernel": f"{ng} work-groups x 8 waves x {iters} x 4 v_mfma_f32_32x32x16_bf16",
+            "read_kernel": f"{nbytes >> 30} GiB read once, {ng2} work-groups x 256 threads, 16-byte loads"}
+
+
+def roofline_of(wl, ev_ms, flops, nbytes):
+    """Roofline block of a workload from its average kernel time per step."""
+    ai = flops / nbytes
+    bound = "hbm" if ai < BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9) else "mfma"
+    if bound == "hbm":
+        gbs = nbytes / (ev_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    else:
+        tf = flops / (ev_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(tf, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(tf / BF16_PEAK_TFLOPS, 4)}
+    roof["traffic"] = load_traffic(wl.name)
+    roof["algorithmic_bytes"] = nbytes
+    roof["algorithmic_flops"] = flops
+    roof["step_ms_events"] = round(ev_ms, 5)
+    return roof
 
 
 def load_traffic(workload_name):
@@ -458,6 +649,18 @@ def load_traffic(workload_name):
     return None
 
 
+def step_record(wl, wall_ms, ev_ms, lat, stats=None):
+    flops, nbytes = algorithmic_flops(wl), algorithmic_bytes(wl)
+    rec = {"workload": wl.name, "ms": round(ev_ms, 5), "wall_ms": round(wall_ms, 5),
+           "TFLOP/s": round(flops / (ev_ms * 1e-3) / 1e12, 1),
+           "mfma_frac": round(flops / (ev_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+           "GB/s": round(nbytes / (ev_ms * 1e-3) / 1e9, 1), "flops": flops, "bytes": nbytes,
+           "latency_ms_per_block": round(lat, 5)}
+    if stats:
+        rec["latency_ms_p10_p90"] = [round(stats["p10"], 5), round(stats["p90"], 5)]
+    return rec
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -466,13 +669,17 @@ def main():
     ap.add_argument("--no-extra", action="store_true", help="headline workload only")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-sweep", action="store_true", help="skip the KV-length sweeps")
-    ap.add_argument("--config", type=int, default=2, help="headline workload index (1-5)")
+    ap.add_argument("--config", type=int, default=5, help="headline workload index (1-5)")
     ap.add_argument("--sweep-only", default=None, metavar="NAME",
                     help="only time the named KV-length sweep point(s), comma-separated (for profiling)")
     ap.add_argument("--varlen-only", action="store_true",
                     help="only time the four-stream step over units of different lengths (for profiling)")
     ap.add_argument("--bwd-only", action="store_true",
                     help="only time the gradients of the whole-sequence workload (for profiling)")
+    ap.add_argument("--replay-only", type=int, default=0, metavar="IDX",
+                    help="only time the streaming replay of workload IDX (1, 3 or 4; for profiling)")
+    ap.add_argument("--solver-only", action="store_true",
+                    help="only time the solver loop, eager and replayed from a HIP graph (for profiling)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (to calibrate "
                          "the FETCH_SIZE / WRITE_SIZE counters against known bytes)")
@@ -499,6 +706,12 @@ def main():
     if args.bwd_only:
         print(json.dumps(backward_timing(dev, steps=args.steps)), flush=True)
         return
+    if args.replay_only:
+        print(json.dumps(replay_timing(args.replay_only, dev)), flush=True)
+        return
+    if args.solver_only:
+        print(json.dumps(solver_loop_timing(dev)), flush=True)
+        return
     if args.varlen_only:
         w2 = inputs.streams_varlen()
         f2, b2 = algorithmic_flops(w2), algorithmic_bytes(w2)
@@ -515,52 +728,62 @@ def main():
         print(json.dumps(run_sweeps(dev, args.steps, points=pts)), flush=True)
         return
 
-    wl = inputs.config(args.config)
-    if wl.kind == "step" and args.config == 2:
-        wl.fuse_append = True  # the per-block step commits its block
+    def workload(idx):
+        w = inputs.config(idx)
+        if w.kind == "step":
+            w.fuse_append = True  # every per-block step commits its block
+        return w
+
+    wl = workload(args.config)
     flops, nbytes = algorithmic_flops(wl), algorithmic_bytes(wl)
     torch.cuda.synchronize()
     lat_stats = {}
     wall_ms, ev_mean, ev_med, _ = time_workload(wl, args.steps, args.warmup, dev, stats=lat_stats)
     tflops = flops / (wall_ms * 1e-3) / 1e12
-    gbs_kernel = nbytes / (ev_mean * 1e-3) / 1e9
-    ai = flops / nbytes
-    bound = "hbm" if ai < BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9) else "mfma"
-    if bound == "hbm":
-        roof = {"bound": "hbm", "achieved": round(gbs_kernel, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(gbs_kernel / HBM_PEAK_GBS, 4)}
-    else:
-        tf_kernel = flops / (ev_mean * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(tf_kernel, 1), "peak": BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(tf_kernel / BF16_PEAK_TFLOPS, 4)}
-    roof["traffic"] = load_traffic(wl.name)
-    roof["algorithmic_bytes"] = nbytes
-    roof["algorithmic_flops"] = flops
-    roof["step_ms_events"] = round(ev_mean, 5)
+    roof = roofline_of(wl, ev_mean, flops, nbytes)
 
-    extra = []
+    extra, oracle_runs = [], []
     if not args.no_extra:
-        for idx in (3, 4, 5, "thinker", "varlen"):
+        for idx in (2, 3, 4, "thinker", "varlen"):
             if idx == args.config:
                 continue
             # "thinker": the interleaved workload with each unit's text
             # segment token-causal; "varlen": four streams each ingesting an
             # interleaved unit of its own length in one step
             w2 = (inputs.thinker_prefill() if idx == "thinker" else inputs.streams_varlen() if idx == "varlen"
-                  else inputs.config(idx))
-            f2, b2 = algorithmic_flops(w2), algorithmic_bytes(w2)
-            wms, emean, emed, _ = time_workload(w2, max(3, args.steps // 5), 2, dev, latency_steps=0)
-            extra.append({"workload": w2.name, "ms": round(emean, 4), "TFLOP/s": round(f2 / (emean * 1e-3) / 1e12, 1),
-                          "mfma_frac": round(f2 / (emean * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
-                          "GB/s": round(b2 / (emean * 1e-3) / 1e9, 1), "flops": f2, "bytes": b2})
+                  else workload(idx))
+            st = {}
+            n_steps = args.steps if w2.kind == "step" and idx == 2 else max(3, args.steps // 5)
+            wms, emean, emed, _ = time_workload(w2, n_steps, 2, dev, latency_steps=n_steps if idx == 2 else 0,
+                                                stats=st if idx == 2 else None)
+            rec = step_record(w2, wms, emean, emed, st if idx == 2 else None)
+            if idx == 2:   # the single-block step: HBM-bound, reported with its roofline
+                rec["roofline"] = roofline_of(w2, emean, algorithmic_flops(w2), algorithmic_bytes(w2))
+            extra.append(rec)
             del w2
             torch.cuda.empty_cache()
-
-    if not args.no_extra:
         extra.append(solver_loop_timing(dev))
         extra.append(backward_timing(dev))
     sweeps = [] if (args.no_extra or args.no_sweep) else run_sweeps(dev, 200)
-    cpu = None if args.no_cpu else cpu_baseline(wl)
+    replays = [] if (args.no_extra or args.no_sweep) else [replay_timing(i, dev) for i in (1, 3, 4)]
+    ceil = None if args.no_extra else ceilings(dev)
+    if ceil is not None:
+        # the headline against the measured ceiling too
+        roof["frac_of_measured_ceiling"] = round(roof["achieved"] / (
+            ceil["mfma_bf16_TFLOP/s"] if roof["bound"] == "mfma" else ceil["hbm_read_GB/s"]), 4)
+        for rec in extra:
+            r2 = rec.get("roofline")
+            if r2:
+                r2["frac_of_measured_ceiling"] = round(r2["achieved"] / (
+                    ceil["mfma_bf16_TFLOP/s"] if r2["bound"] == "mfma" else ceil["hbm_read_GB/s"]), 4)
+    cpu = None
+    if not args.no_cpu:
+        cpu = oracle_sample(wl)
+        if not args.no_extra:
+            for idx in (1, 2, 3, 4):
+                if idx != args.config:
+                    oracle_runs.append(oracle_sample(inputs.config(idx)))
+            oracle_runs.append(cpu)
     line = {
         "metric": METRIC,
         "value": round(tflops, 2),
@@ -583,8 +806,11 @@ def main():
         "latency_ms_p10_p90": [round(lat_stats["p10"], 5), round(lat_stats["p90"], 5)],
         "roofline": roof,
         "cpu_baseline": cpu,
+        "ceilings": ceil,
         "extra": extra,
         "sweeps": sweeps,
+        "replays": replays,
+        "oracle_by_workload": oracle_runs,
         "gpu": torch.cuda.get_device_name(0),
     }
     print(json.dumps(line), flush=True)

@@ -82,7 +82,7 @@
 extern "C" {
 #endif
 
-#define WS_ABI_VERSION 4
+#define WS_ABI_VERSION 5
 #define WS_PAGE_SIZE 64
 
 typedef enum {
@@ -191,9 +191,11 @@ int ws_kv_append(const ws_paged_kv *kv, int32_t batch,
  *                are ignored.
  * new_len x (num_q_heads / num_kv_heads) must not exceed 2^30 (WS_ERR_SHAPE).
  * The library splits long caches into KV partitions merged by a second
- * launch; the environment variable WS_SPLITS (1..32), read at each call,
- * overrides the chosen partition count (for tuning; ws_workspace_bytes
- * follows the same setting, so read both under the same environment).
+ * launch.  The partition count is planned for the compute units of the
+ * current device (queried once per device; ws_step_plan shows the plan for
+ * any count).  The environment variable WS_SPLITS (1..32) overrides it for
+ * tuning; it is read once per process, at the first call that plans a
+ * step, so workspace queries and calls always agree.
  * Errors: WS_ERR_NULL, WS_ERR_SHAPE, WS_ERR_UNSUPPORTED, WS_ERR_ALIGN,
  * WS_ERR_HEADS, WS_ERR_CAPACITY, WS_ERR_PAGE, WS_ERR_WORKSPACE, WS_ERR_HIP.
  */
@@ -290,8 +292,9 @@ int ws_block_causal_attn_fwd_varlen(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v
 /*
  * ws_step_workspace_bytes_varlen -- device workspace bytes that
  * ws_block_causal_attn_fwd_varlen needs for these host arrays (int32
- * [batch] each; the same WS_SPLITS setting applies).  0 when none is needed
- * or when an argument is invalid (the call itself then reports why).
+ * [batch] each), planned for the current device.  0 when none is needed,
+ * when an argument is invalid (the call itself then reports why) or when
+ * no device is available.
  */
 size_t ws_step_workspace_bytes_varlen(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
                                       int32_t new_len, const int32_t *cache_lens_host,
@@ -368,12 +371,30 @@ int ws_block_causal_prefill_bwd(ws_tensor4 q, ws_tensor4 k, ws_tensor4 v, ws_ten
  * Workspace bytes ws_block_causal_attn_fwd (and its _text variant) needs
  * for this shape (op =
  * WS_OP_STEP; num_kv_heads = the cache's; max_k = largest cache_lens[b] +
- * new_len).  WS_OP_PREFILL returns 0.  WS_OP_PREFILL_BWD (max_q = max_k =
- * seq_len): the bytes ws_block_causal_prefill_bwd needs.  Pure host
- * arithmetic; returns 0 for invalid arguments.
+ * new_len), planned for the current device's compute units (0 when no
+ * device is available).  WS_OP_PREFILL returns 0.  WS_OP_PREFILL_BWD
+ * (max_q = max_k = seq_len): the bytes ws_block_causal_prefill_bwd needs
+ * (pure host arithmetic).  Returns 0 for invalid arguments.
  */
 size_t ws_workspace_bytes(int32_t op, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
                           int32_t max_q, int32_t max_k);
+
+/*
+ * ws_step_plan -- the launch plan of a streaming step (host only; nothing
+ * is enqueued).  Work items are (stream, KV head, 256-row query tile, KV
+ * split); the plan picks the KV split count for num_cus compute units
+ * (0: the current device's) and reports the workspace the step needs:
+ * the value ws_block_causal_attn_fwd(_text) (new_lens_host NULL) or
+ * ws_block_causal_attn_fwd_varlen (new_lens_host: int32 [batch]) checks
+ * on a device with that many compute units.
+ *   cache_lens_host: int32 [batch]
+ *   num_splits, workspace_bytes: outputs
+ * Errors: WS_ERR_NULL, WS_ERR_SHAPE (sizes, a length outside its range),
+ * WS_ERR_HEADS, WS_ERR_HIP (num_cus == 0 and no device).
+ */
+int ws_step_plan(int32_t num_cus, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                 int32_t new_len, const int32_t *cache_lens_host, const int32_t *new_lens_host,
+                 int32_t *num_splits, size_t *workspace_bytes);
 
 #ifdef __cplusplus
 }

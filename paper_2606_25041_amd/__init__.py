@@ -16,6 +16,7 @@ lengths padded to a common one)
   block_causal_prefill_bwd(q, k, v, o, dout, lse, block_offsets, ...)
   workspace_bytes(op, batch, num_q_heads, num_kv_heads, max_q, max_k)
   step_workspace_bytes_varlen(batch, num_q_heads, num_kv_heads, new_len, cache_lens, new_lens)
+  step_plan(batch, num_q_heads, num_kv_heads, new_len, cache_lens, new_lens=None, num_cus=0)
 """
 import ctypes
 import math
@@ -27,7 +28,7 @@ from . import build as _build
 
 __all__ = ["WsError", "PagedCache", "kv_append", "block_causal_attn_fwd",
            "block_causal_prefill", "block_causal_prefill_bwd", "workspace_bytes",
-           "step_workspace_bytes_varlen", "library",
+           "step_workspace_bytes_varlen", "step_plan", "library",
            "abi_version", "WS_OP_STEP", "WS_OP_PREFILL", "WS_OP_PREFILL_BWD", "PAGE_SIZE"]
 
 WS_DTYPE_BF16, WS_DTYPE_F32 = 1, 2
@@ -107,7 +108,10 @@ def library():
         lib.ws_block_causal_prefill_bwd.argtypes = [
             Tensor4, Tensor4, Tensor4, Tensor4, Tensor4, P, P, P, P, P, I32, I32, I32, I32, I32, I32, F,
             Tensor4, Tensor4, Tensor4, P, ctypes.c_size_t, P]
-        if lib.ws_abi_version() != 4:
+        lib.ws_step_plan.restype = ctypes.c_int
+        lib.ws_step_plan.argtypes = [I32, I32, I32, I32, I32, P, P, ctypes.POINTER(I32),
+                                     ctypes.POINTER(ctypes.c_size_t)]
+        if lib.ws_abi_version() != 5:
             raise RuntimeError("libwsattn.so ABI version mismatch")
         _LIB = lib
     return _LIB
@@ -218,6 +222,17 @@ def step_workspace_bytes_varlen(batch, num_q_heads, num_kv_heads, new_len, cache
     nh = torch.as_tensor(new_lens, dtype=torch.int32).cpu().contiguous()
     return library().ws_step_workspace_bytes_varlen(batch, num_q_heads, num_kv_heads, new_len, ch.data_ptr(),
                                                     nh.data_ptr())
+
+
+def step_plan(batch, num_q_heads, num_kv_heads, new_len, cache_lens, new_lens=None, num_cus=0):
+    """(KV split count, workspace bytes) of a step planned for num_cus
+    compute units (0: the current device's)."""
+    ch = torch.as_tensor(cache_lens, dtype=torch.int32).cpu().contiguous()
+    nh = None if new_lens is None else torch.as_tensor(new_lens, dtype=torch.int32).cpu().contiguous()
+    ns, nbytes = ctypes.c_int32(0), ctypes.c_size_t(0)
+    _check(library().ws_step_plan(num_cus, batch, num_q_heads, num_kv_heads, new_len, ch.data_ptr(),
+                                  _ptr(nh), ctypes.byref(ns), ctypes.byref(nbytes)))
+    return ns.value, nbytes.value
 
 
 def kv_append(cache, cache_lens, k_new, v_new, new_lens=None):

@@ -54,6 +54,21 @@ def build(verbose=False):
     return LIB
 
 
+CEIL_SRC = os.path.join(CSRC, "ws_ceilings.hip")
+CEIL_LIB = os.path.join(HERE, "libwsceil.so")
+
+
+def build_ceilings(verbose=False):
+    """The ceiling microbenchmarks (MFMA loop, streaming read) that the
+    benchmark runs beside the attention kernels, as libwsceil.so."""
+    msgs = _run([hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared", "-Wall"]
+                + KERNEL_FLAGS + [CEIL_SRC, "-o", CEIL_LIB + ".tmp"])
+    if verbose and msgs:
+        print("\n".join(msgs))
+    os.replace(CEIL_LIB + ".tmp", CEIL_LIB)
+    return CEIL_LIB
+
+
 def is_stale():
     if not os.path.exists(LIB):
         return True
@@ -63,3 +78,4 @@ def is_stale():
 
 if __name__ == "__main__":
     print(build(verbose=True))
+    print(build_ceilings(verbose=True))

@@ -31,7 +31,6 @@ int ok() {
     return WS_OK;
 }
 
-constexpr int NUM_CUS = 256;            // MI355X compute units
 constexpr int WS_MAX_SPLITS = ws::MAX_SPLITS;
 // packed query rows of one (stream, KV head) in a step: G x new_len (the
 // kernels index them in 32-bit arithmetic)
@@ -42,6 +41,17 @@ int env_int(const char *name, int dflt) {
     const char *s = std::getenv(name);
     if (!s || !*s) return dflt;
     return std::atoi(s);
+}
+
+// Tuning override of the KV split count (WS_SPLITS = 1..32), read once, at
+// the first call that plans a step, and fixed for the rest of the process,
+// so workspace queries and calls always agree.  0: no override.
+int split_override() {
+    static const int s = [] {
+        const int v = env_int("WS_SPLITS", 0);
+        return v <= 0 ? 0 : v > WS_MAX_SPLITS ? WS_MAX_SPLITS : v;
+    }();
+    return s;
 }
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
@@ -128,7 +138,7 @@ constexpr int64_t SPLIT_FIXED_TILES = 4;
 // when the items do not fill the last round (a batch of 3 or 5 long
 // streams, or new blocks of different lengths, nl != NULL, whose tiles of
 // padding only do no work).
-StepPlan plan_step(int batch, int hq, int hkv, int lq, int64_t max_k, const int32_t *nl = nullptr) {
+StepPlan plan_step(int num_cus, int batch, int hq, int hkv, int lq, int64_t max_k, const int32_t *nl = nullptr) {
     StepPlan p;
     p.shape = default_shape();
     const int64_t qt = p.shape.qtile();
@@ -142,7 +152,7 @@ StepPlan plan_step(int batch, int hq, int hkv, int lq, int64_t max_k, const int3
         base *= hkv;
     }
     const int64_t ntiles = (max_k + 63) / 64;
-    const int64_t slots = (int64_t)NUM_CUS * p.shape.groups_per_cu();
+    const int64_t slots = (int64_t)num_cus * p.shape.groups_per_cu();
     int64_t cap = ntiles / 2;
     if (cap > WS_MAX_SPLITS) cap = WS_MAX_SPLITS;
     if (cap < 1) cap = 1;
@@ -167,7 +177,7 @@ StepPlan plan_step(int batch, int hq, int hkv, int lq, int64_t max_k, const int3
             const int64_t g = w / P, kvh = g / batch, b = g % batch;
             return (kvh * pre[batch] + pre[b]) * s + std::min(w - g * P, (pre[b + 1] - pre[b]) * s);
         };
-        const int64_t per_cu = slots / ws::NUM_XCD;
+        const int64_t per_cu = std::max<int64_t>(1, slots / ws::NUM_XCD);
         int64_t rounds = 0;
         for (int64_t x = 0; x < ws::NUM_XCD; ++x) {
             const int64_t c = real_before((x + 1) * per) - real_before(x * per);
@@ -185,8 +195,7 @@ StepPlan plan_step(int batch, int hq, int hkv, int lq, int64_t max_k, const int3
         while (50 * cost(best) > 51 * lo) ++best;
         if (10 * cost(best) < 9 * cost(ns)) ns = best;
     }
-    const int s_env = env_int("WS_SPLITS", 0);
-    if (s_env > 0) ns = s_env > WS_MAX_SPLITS ? WS_MAX_SPLITS : s_env;
+    if (const int s_ov = split_override()) ns = s_ov;
     p.nsplit = (int)ns;
     return p;
 }
@@ -281,7 +290,9 @@ size_t ws_workspace_bytes(int32_t op, int32_t batch, int32_t num_q_heads, int32_
         max_k < max_q)
         return 0;
     if ((int64_t)(num_q_heads / num_kv_heads) * max_q > WS_MAX_STEP_ROWS) return 0;
-    const StepPlan p = plan_step(batch, num_q_heads, num_kv_heads, max_q, max_k);
+    int cus = 0;
+    if (ws::current_device_cus(&cus)) return 0;
+    const StepPlan p = plan_step(cus, batch, num_q_heads, num_kv_heads, max_q, max_k);
     return step_workspace(p, batch, num_q_heads, num_kv_heads, max_q);
 }
 
@@ -298,8 +309,40 @@ size_t ws_step_workspace_bytes_varlen(int32_t batch, int32_t num_q_heads, int32_
         if (k > max_k) max_k = k;
     }
     if (max_k > INT32_MAX) return 0;
-    const StepPlan p = plan_step(batch, num_q_heads, num_kv_heads, new_len, max_k, new_lens_host);
+    int cus = 0;
+    if (ws::current_device_cus(&cus)) return 0;
+    const StepPlan p = plan_step(cus, batch, num_q_heads, num_kv_heads, new_len, max_k, new_lens_host);
     return step_workspace(p, batch, num_q_heads, num_kv_heads, new_len);
+}
+
+int ws_step_plan(int32_t num_cus, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t new_len,
+                 const int32_t *cache_lens_host, const int32_t *new_lens_host, int32_t *num_splits,
+                 size_t *workspace_bytes) {
+    if (!cache_lens_host || !num_splits || !workspace_bytes) return fail(WS_ERR_NULL, "NULL argument");
+    if (num_cus < 0 || batch <= 0 || new_len <= 0 || num_q_heads <= 0 || num_kv_heads <= 0)
+        return fail(WS_ERR_SHAPE, "num_cus %d, batch %d, new_len %d, heads %d/%d", (int)num_cus, (int)batch,
+                    (int)new_len, (int)num_q_heads, (int)num_kv_heads);
+    if (num_q_heads % num_kv_heads)
+        return fail(WS_ERR_HEADS, "num_q_heads %d not a multiple of num_kv_heads %d", (int)num_q_heads,
+                    (int)num_kv_heads);
+    if ((int64_t)(num_q_heads / num_kv_heads) * new_len > WS_MAX_STEP_ROWS)
+        return fail(WS_ERR_SHAPE, "new_len x query heads per KV head exceeds %lld", (long long)WS_MAX_STEP_ROWS);
+    int64_t max_k = 0;
+    for (int b = 0; b < batch; ++b) {
+        if (cache_lens_host[b] < 0) return fail(WS_ERR_SHAPE, "cache_lens[%d] = %d", b, (int)cache_lens_host[b]);
+        if (new_lens_host && (new_lens_host[b] < 1 || new_lens_host[b] > new_len))
+            return fail(WS_ERR_SHAPE, "new_lens[%d] = %d outside [1, new_len %d]", b, (int)new_lens_host[b],
+                        (int)new_len);
+        max_k = std::max(max_k, (int64_t)cache_lens_host[b] + (new_lens_host ? new_lens_host[b] : new_len));
+    }
+    if (max_k > INT32_MAX) return fail(WS_ERR_SHAPE, "too many keys");
+    int cus = num_cus;
+    if (cus == 0)
+        if (int e = ws::current_device_cus(&cus)) return fail(WS_ERR_HIP, "no device to plan for (hip error %d)", e);
+    const StepPlan p = plan_step(cus, batch, num_q_heads, num_kv_heads, new_len, max_k, new_lens_host);
+    *num_splits = p.nsplit;
+    *workspace_bytes = step_workspace(p, batch, num_q_heads, num_kv_heads, new_len);
+    return ok();
 }
 
 int ws_kv_append(const ws_paged_kv *kv, int32_t batch, const int32_t *cache_lens_host,
@@ -527,7 +570,10 @@ int step_impl(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_k
                             (int)new_len);
     if ((int64_t)(num_q_heads / kv->num_kv_heads) * new_len > WS_MAX_STEP_ROWS)
         return fail(WS_ERR_SHAPE, "new_len x query heads per KV head exceeds %lld", (long long)WS_MAX_STEP_ROWS);
-    const StepPlan plan = plan_step(batch, num_q_heads, kv->num_kv_heads, new_len, max_k, nl_host);
+    int cus = 0;
+    if (int e = ws::current_device_cus(&cus))
+        return fail(WS_ERR_HIP, "cannot query the device's compute units (hip error %d)", e);
+    const StepPlan plan = plan_step(cus, batch, num_q_heads, kv->num_kv_heads, new_len, max_k, nl_host);
     const size_t need_ws = step_workspace(plan, batch, num_q_heads, kv->num_kv_heads, new_len);
     if (need_ws > 0 && (!workspace || workspace_bytes < need_ws || !aligned16(workspace)))
         return fail(WS_ERR_WORKSPACE, "workspace needs %zu bytes (16-byte aligned), got %zu", need_ws,

@@ -162,5 +162,8 @@ int launch_combine(const AttnArgs &a, int head_dim, void *stream);
 int launch_append(const AppendArgs &a, void *stream);
 // prep (row sums, key ends), then dQ and dK/dV; 0 or a HIP error code
 int launch_prefill_bwd(const BwdArgs &a, int head_dim, void *stream);
+// Compute units of the current HIP device (queried once per device, then
+// cached): 0 and *cus set, or a HIP error code (e.g. no device).
+int current_device_cus(int *cus);
 
 }  // namespace ws

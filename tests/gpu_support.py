@@ -121,3 +121,47 @@ def assert_close(stats):
     assert stats["mean_abs"] <= MEAN_ABS, stats
     if "lse_max_abs" in stats:
         assert stats["lse_max_abs"] <= LSE_ABS, stats
+
+
+def coverage_rows_prefill(g, B, Hq, L, must=()):
+    """(b, h, i) rows for a full-size prefill check: one row of every 32-row
+    block of every (stream, query head), which is every wave of every work
+    item (a work item is one query head's 256-row tile): the first row of a
+    tile's first block, the last row of its last block, a random row of the
+    others; plus the given rows."""
+    rows = {tuple(int(x) for x in r) for r in must}
+    for b in range(B):
+        for h in range(Hq):
+            for k in range(-(-L // 32)):
+                lo, hi = 32 * k, min(32 * k + 32, L)
+                if k % 8 == 0:
+                    i = lo
+                elif k % 8 == 7 or hi == L:
+                    i = hi - 1
+                else:
+                    i = int(g.integers(lo, hi))
+                rows.add((b, h, i))
+    return np.array(sorted(rows), dtype=np.int32)
+
+
+def coverage_rows_step(g, B, Hq, Hkv, Lq, must=(), new_lens=None):
+    """(b, h, t) rows for a full-size step check.  A step packs the G query
+    heads of a KV head into one row space, row p = t * G + hh; one row of
+    every 32-row block of it per (stream, KV head), chosen as in
+    ``coverage_rows_prefill`` (each 256-row tile's first and last row).
+    Every such row sees every KV split.  new_lens: only real tokens."""
+    G = Hq // Hkv
+    rows = {tuple(int(x) for x in r) for r in must}
+    for b in range(B):
+        n = G * (Lq if new_lens is None else int(new_lens[b]))
+        for kvh in range(Hkv):
+            for k in range(-(-n // 32)):
+                lo, hi = 32 * k, min(32 * k + 32, n)
+                if k % 8 == 0:
+                    p = lo
+                elif k % 8 == 7 or hi == n:
+                    p = hi - 1
+                else:
+                    p = int(g.integers(lo, hi))
+                rows.add((b, kvh * G + p % G, p // G))
+    return np.array(sorted(rows), dtype=np.int32)

@@ -43,12 +43,32 @@ def test_exports_every_declared_symbol(lib):
     assert {"ws_kv_append", "ws_block_causal_attn_fwd", "ws_block_causal_prefill",
             "ws_block_causal_attn_fwd_text", "ws_block_causal_prefill_text", "ws_block_causal_prefill_bwd",
             "ws_block_causal_attn_fwd_varlen", "ws_kv_append_varlen", "ws_step_workspace_bytes_varlen",
-            "ws_workspace_bytes", "ws_abi_version", "ws_status_string", "ws_last_error"} <= set(names)
+            "ws_workspace_bytes", "ws_step_plan", "ws_abi_version", "ws_status_string",
+            "ws_last_error"} <= set(names)
     for name in names:
         assert hasattr(lib, name), name
-    assert lib.ws_abi_version() == 4
+    assert lib.ws_abi_version() == 5
     assert lib.ws_status_string(0) == b"WS_OK"
     assert lib.ws_status_string(10) == b"WS_ERR_HIP"
+
+
+def test_ceilings_library_exports_every_declared_symbol():
+    """libwsceil.so (the benchmark's MFMA and HBM-read ceilings) loads and
+    exports what include/ws_ceilings.h declares."""
+    if not os.path.exists(wsbuild.CEIL_LIB):
+        wsbuild.build_ceilings()
+    lib = ctypes.CDLL(wsbuild.CEIL_LIB)
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "ws_ceilings.h")).read(), flags=re.S)
+    names = sorted(set(re.findall(r"\b(wsc_[a-z0-9_]+)\s*\(", text)))
+    assert names == ["wsc_mfma_loop", "wsc_stream_read"]
+    for name in names:
+        assert hasattr(lib, name), name
+    # argument checks fail before anything is launched
+    lib.wsc_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int32,
+                                    ctypes.c_void_p]
+    lib.wsc_mfma_loop.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p]
+    assert lib.wsc_stream_read(FAKE, 17, FAKE, 1, None) != 0
+    assert lib.wsc_mfma_loop(None, 1, 1, None) != 0
 
 
 def t4(ptr=FAKE, dtype=ws.WS_DTYPE_BF16, sb=0, st=0, sh=0, d=128, L=16, H=4):
@@ -115,12 +135,13 @@ def test_step_errors(lib):
     assert step_call(lib, h4) == 6
     h5 = Host(lens=(10, -1))
     assert step_call(lib, h5) == 2
+    # A call that passes every argument check plans for the device's compute
+    # units next; with no device here that query fails (the workspace checks
+    # that follow run in the GPU tests).
     hw = Host(lens=(10, 200))            # 216 keys: the plan splits the KV range
-    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 2, 4, 2, 16, 216) > 0
-    assert step_call(lib, hw, wsp=None) == 9
-    assert step_call(lib, hw, wsb=16) == 9
-    assert step_call(lib, hw, wsp=FAKE + 4) == 9                       # misaligned workspace
-    assert lib.ws_last_error() != b""
+    assert plan(lib, 256, 2, 4, 2, 16, [10, 200])[1] > 0
+    assert step_call(lib, hw, wsp=None) == 10
+    assert b"compute units" in lib.ws_last_error()
 
 
 def test_step_capacity_counts_fused_append(lib):
@@ -240,33 +261,49 @@ def test_step_varlen_capacity_counts_real_tokens(lib):
     # 4 pages hold 256 tokens: stream 1 (250 cached) can commit 6 new tokens, not 7
     h = Host(lens=(10, 250))
     assert step_varlen_call(lib, h, [16, 7], flags=ws.WS_FUSE_APPEND) == 7
-    # 6 fits and reaches the workspace check (the 256-key range is split)
-    assert step_varlen_call(lib, h, [16, 6], flags=ws.WS_FUSE_APPEND, wsb=16) == 9
+    # 6 fits and passes every argument check (it then plans for the device)
+    assert step_varlen_call(lib, h, [16, 6], flags=ws.WS_FUSE_APPEND, wsb=16) == 10
 
 
-def test_step_workspace_bytes_varlen(lib):
-    def wsv(B, hq, hkv, lq, lens, nls):
-        ch = np.ascontiguousarray(np.asarray(lens, np.int32))
-        nh = np.ascontiguousarray(np.asarray(nls, np.int32))
-        return lib.ws_step_workspace_bytes_varlen(B, hq, hkv, lq, ch.ctypes.data, nh.ctypes.data)
+def plan(lib, cus, B, hq, hkv, lq, lens, nls=None):
+    """(status, workspace bytes, splits) from ws_step_plan."""
+    ch = np.ascontiguousarray(np.asarray(lens, np.int32))
+    nh = None if nls is None else np.ascontiguousarray(np.asarray(nls, np.int32))
+    ns, nbytes = ctypes.c_int32(-1), ctypes.c_size_t(0)
+    rc = lib.ws_step_plan(cus, B, hq, hkv, lq, ch.ctypes.data, None if nh is None else nh.ctypes.data,
+                          ctypes.byref(ns), ctypes.byref(nbytes))
+    return rc, nbytes.value, ns.value
+
+
+def test_step_plan_workspace_and_errors(lib):
     lens = [131072] * 4
-    # equal lengths: the plain step's plan
+    ws_of = lambda *a, **k: plan(lib, 256, *a, **k)[1]
+    # equal lengths given as lengths: the plain step's plan
     for lq, c in ((512, 131072), (243, 131072), (8, 131072), (256, 4096)):
-        assert wsv(4, 64, 8, lq, [c] * 4, [lq] * 4) == lib.ws_workspace_bytes(ws.WS_OP_STEP, 4, 64, 8, lq, c + lq)
+        assert ws_of(4, 64, 8, lq, [c] * 4, [lq] * 4) == ws_of(4, 64, 8, lq, [c] * 4)
     # four long streams padded to 243 tokens fill the CUs exactly (no split,
     # no workspace); with their real lengths 72 of the 256 work-groups hold
     # padding only, and the KV range is split instead
-    assert wsv(4, 64, 8, 243, lens, [243] * 4) == 0
-    assert wsv(4, 64, 8, 243, lens, [145, 110, 163, 243]) > 0
+    assert ws_of(4, 64, 8, 243, lens, [243] * 4) == 0
+    assert ws_of(4, 64, 8, 243, lens, [145, 110, 163, 243]) > 0
     # a batch of 3 long 512-token blocks (384 work-groups: 1.5 rounds) splits too
-    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 3, 64, 8, 512, 131072 + 512) > 0
-    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 4, 64, 8, 512, 131072 + 512) == 0
-    # invalid arguments give 0
-    assert wsv(4, 64, 8, 243, lens, [145, 0, 163, 243]) == 0
-    assert wsv(4, 64, 8, 243, lens, [145, 244, 163, 243]) == 0
-    assert wsv(4, 64, 8, 243, [131072, -1, 5, 5], [145, 110, 163, 243]) == 0
-    assert wsv(4, 64, 7, 243, lens, [145, 110, 163, 243]) == 0
-    assert lib.ws_step_workspace_bytes_varlen(4, 64, 8, 243, None, None) == 0
+    assert ws_of(3, 64, 8, 512, lens[:3]) > 0
+    assert ws_of(4, 64, 8, 512, lens) == 0
+    # invalid arguments
+    assert plan(lib, 256, 4, 64, 8, 243, lens, [145, 0, 163, 243])[0] == 2
+    assert plan(lib, 256, 4, 64, 8, 243, lens, [145, 244, 163, 243])[0] == 2
+    assert plan(lib, 256, 4, 64, 8, 243, [131072, -1, 5, 5], [145, 110, 163, 243])[0] == 2
+    assert plan(lib, 256, 4, 64, 7, 243, lens)[0] == 8
+    assert plan(lib, -1, 4, 64, 8, 243, lens)[0] == 2
+    ns, nb = ctypes.c_int32(0), ctypes.c_size_t(0)
+    assert lib.ws_step_plan(256, 4, 64, 8, 243, None, None, ctypes.byref(ns), ctypes.byref(nb)) == 1
+    # no device here: planning for "the current device" fails, and the
+    # device-planned workspace queries return 0
+    assert plan(lib, 0, 1, 24, 24, 256, [4096])[0] == 10
+    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 1, 24, 24, 256, 4352) == 0
+    ch = np.array([4096], np.int32)
+    nh = np.array([256], np.int32)
+    assert lib.ws_step_workspace_bytes_varlen(1, 24, 24, 256, ch.ctypes.data, nh.ctypes.data) == 0
 
 
 def append_varlen_call(lib, h, new_lens, Ln=16, nl_dev=FAKE, kn=None):
@@ -346,28 +383,31 @@ def test_empty_calls_are_ok(lib):
 
 def test_workspace_bytes(lib):
     # a single 256-row tile per head needs KV splits (and partials) to fill the chip
-    n = lib.ws_workspace_bytes(ws.WS_OP_STEP, 1, 24, 24, 256, 4352)
+    n = plan(lib, 256, 1, 24, 24, 256, [4096])[1]
     assert n > 0 and n % (24 * 256 * 130 * 4) == 0
     # enough work items already: no splits, no workspace
-    assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 4, 64, 8, 512, 131584) == 0
+    assert plan(lib, 256, 4, 64, 8, 512, [131072] * 4)[1] == 0
     # a 16-token block of 8 query heads per KV head packs into one 128-row
     # tile per (stream, KV head): 32 tiles, so the long cache is split
-    n16 = lib.ws_workspace_bytes(ws.WS_OP_STEP, 4, 64, 8, 16, 131088)
+    n16 = plan(lib, 256, 4, 64, 8, 16, [131072] * 4)[1]
     assert n16 > 0 and n16 % (4 * 8 * 128 * 130 * 4) == 0
+    # on a partition of 32 compute units the 24 tiles of the headline step
+    # need fewer splits
+    assert 1 < plan(lib, 32, 1, 24, 24, 256, [4096])[2] < plan(lib, 256, 1, 24, 24, 256, [4096])[2]
     assert lib.ws_workspace_bytes(ws.WS_OP_PREFILL, 2, 32, 8, 16384, 16384) == 0
     assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 0, 24, 24, 256, 4352) == 0
     assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 1, 24, 5, 256, 4352) == 0   # 24 % 5 != 0
     assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 1, 24, 0, 256, 4352) == 0
 
 
-def _split_model(B, hq, hkv, lq, lens, nls):
+def _split_model(B, hq, hkv, lq, lens, nls, slots=256):
     """The documented split rule, written out by brute force: the default
-    (the largest split count whose work-groups fit one round of 256 CUs), and
+    (the largest split count whose work-groups fit one round of the CUs), and
     rounds(s) x (ceil(tiles / s) + 4) counted per XCD over the real items of
     the launch order (groups KV-head-major for blocks of different lengths),
     the fewest splits within 2 % of its minimum taking over when that is
     more than 10 % cheaper than the default.  Returns the split count."""
-    qt, slots, xcds, fixed = 256, 256, 8, 4
+    qt, xcds, fixed = 256, 8, 4
     G = hq // hkv
     nqt = -(-G * lq // qt)
     real = [-(-G * n // qt) for n in nls] if nls is not None else [nqt] * B
@@ -387,7 +427,7 @@ def _split_model(B, hq, hkv, lq, lens, nls):
             lo, hi = g * P, g * P + real[g % B] * s
             for x in range(xcds):
                 cnt[x] += max(0, min(hi, (x + 1) * per) - max(lo, x * per))
-        return max(-(-c // (slots // xcds)) for c in cnt) * per_split
+        return max(-(-c // max(1, slots // xcds)) for c in cnt) * per_split
 
     ns = min(slots // base if base < slots else 1, cap)
     lo = min(cost(s) for s in range(1, cap + 1))
@@ -397,10 +437,11 @@ def _split_model(B, hq, hkv, lq, lens, nls):
     return best if 10 * cost(best) < 9 * cost(ns) else ns
 
 
-def test_split_planner_matches_its_rule(lib):
-    """The library's split count (read back from the workspace size) equals
-    the rule computed by brute force, for equal and for different new-block
-    lengths, on random shapes."""
+@pytest.mark.parametrize("cus", [256, 32])
+def test_split_planner_matches_its_rule(lib, cus):
+    """The library's split count and workspace equal the rule computed by
+    brute force, for equal and for different new-block lengths, on random
+    shapes, for the full chip (256 compute units) and a 32-unit partition."""
     rng = np.random.default_rng(17)
     for _ in range(150):
         hkv = int(rng.choice([1, 2, 4, 8, 16]))
@@ -412,10 +453,8 @@ def test_split_planner_matches_its_rule(lib):
         rows = -(-G * lq // 32) * 32
         unit = B * hkv * rows * 130 * 4
         for var in (False, True):
-            if var:
-                ch, nh = np.array(lens, np.int32), np.array(nls, np.int32)
-                got = lib.ws_step_workspace_bytes_varlen(B, hkv * G, hkv, lq, ch.ctypes.data, nh.ctypes.data)
-            else:
-                got = lib.ws_workspace_bytes(ws.WS_OP_STEP, B, hkv * G, hkv, lq, max(lens) + lq)
-            ns = _split_model(B, hkv * G, hkv, lq, lens, nls if var else None)
+            rc, got, ns_lib = plan(lib, cus, B, hkv * G, hkv, lq, lens, nls if var else None)
+            assert rc == 0
+            ns = _split_model(B, hkv * G, hkv, lq, lens, nls if var else None, slots=cus)
+            assert ns_lib == ns, (cus, B, hkv * G, hkv, lq, lens, nls, var, ns, ns_lib)
             assert got == (0 if ns == 1 else ns * unit), (B, hkv * G, hkv, lq, lens, nls, var, ns, got)

@@ -74,3 +74,21 @@ def test_algorithmic_bytes_terms():
     h = inputs.config(2)
     h.fuse_append = True
     assert bench.algorithmic_bytes(h) == 59768832
+
+
+def test_oracle_sample_row_keys_match_brute_force():
+    """The per-row key counts behind the oracle sample's TFLOP/s equal the
+    masking rule counted key by key (block-causal, no segments)."""
+    pf = _small_cases()[3]
+    rows = inputs.sample_rows(np.random.default_rng(3), pf.B, pf.Hq, pf.Lq, 40)
+    got = bench.row_key_counts(pf, rows)
+    for (b, h, i), n in zip(rows, got):
+        off = [int(x) for x in pf.offsets[b]]
+        blk = max(k for k in range(len(off) - 1) if off[k] <= i < off[k + 1])
+        assert n == sum(1 for j in range(pf.Lq) if j < off[blk + 1]), (b, h, i)
+    st = _small_cases()[0]
+    rows = inputs.sample_rows(np.random.default_rng(4), st.B, st.Hq, st.Lq, 20)
+    assert list(bench.row_key_counts(st, rows)) == [int(st.cache_lens[b]) + st.Lq for b, _, _ in rows]
+    # a whole workload's rows sum to its visible pairs
+    all_rows = np.array([(b, h, i) for b in range(pf.B) for h in range(pf.Hq) for i in range(pf.Lq)])
+    assert int(bench.row_key_counts(pf, all_rows).sum()) == pf.Hq * sum(bench.visible_pairs(pf))

@@ -119,47 +119,58 @@ def test_step_mha_f32_out():
 
 
 # ---------------------------------------------------------------------------
-# the five named workloads at full size (sampled rows)
+# the five named workloads at full size
 
-def _sampled(wl, cache, must, n=48, seed=5):
-    g = np.random.default_rng(seed)
-    rows = inputs.sample_rows(g, wl.B, wl.Hq, wl.Lq, n, must=must)
-    gs.say(f"[gpu] {wl.name}: full size, {len(rows)} sampled rows")
+def _covered(wl, cache, rows):
+    """Full-size run against the oracle on the given rows (computed one by
+    one by the oracle); every output must be finite (NaN-filled unused pool
+    pages never leak)."""
+    gs.say(f"[gpu] {wl.name}: full size, {len(rows)} rows")
     out, lse = gs.run_gpu(wl, cache=cache)
     torch.cuda.synchronize()
     ref, ref_lse = gs.run_oracle(wl, rows=rows)
     stats = gs.compare(out, lse, ref, ref_lse, rows=rows)
     gs.assert_close(stats)
-    # every output finite (no NaN from unused pool pages)
     assert torch.isfinite(out).all()
-    return stats
+    return out, stats
 
 
 def test_config2_step_full_size():
+    """The headline step at full size (MHA 24 x 128, 256 new tokens, 4096
+    cached, 10 KV splits), committed in the same launch as the benchmark
+    runs it: every output element against the oracle."""
     wl = inputs.config(2)
-    wl.fuse_append = True   # as the benchmark runs it (the block is committed in the same launch)
+    wl.fuse_append = True
     cache = gs.device_cache(wl, wl.cache_lens, fill_on_gpu=True)
-    _sampled(wl, cache, must=[(0, 0, 0), (0, 23, 255), (0, 11, 128), (0, 5, 63)])
+    ns, _ = ws.step_plan(wl.B, wl.Hq, wl.Hkv, wl.Lq, wl.cache_lens)
+    gs.say(f"[gpu] {wl.name}: full size, every output ({ns} KV splits)")
+    _check_full(wl, cache=cache)
 
 
 def test_config3_prefill_full_size():
     wl = inputs.config(3)
-    _sampled(wl, None, must=[(0, 0, 0), (1, 31, 16383), (0, 7, 255), (1, 8, 256), (0, 16, 8191)])
+    rows = gs.coverage_rows_prefill(np.random.default_rng(5), wl.B, wl.Hq, wl.Lq,
+                                    must=[(1, 31, 16383), (0, 7, 255), (1, 8, 256), (0, 16, 8191)])
+    _covered(wl, None, rows)
 
 
 def test_config4_interleaved_full_size():
     wl = inputs.config(4)
     cache = gs.device_cache(wl, [wl.Lq], fill_on_gpu=True)
     offs = wl.offsets[0]
-    must = [(0, 0, int(offs[j])) for j in (1, 50, 127)] + [(0, 39, int(offs[j]) - 1) for j in (2, 64, 128)]
-    _sampled(wl, cache, must=must)
+    # every block's first and last row in some head, on top of the coverage
+    must = [(0, j % wl.Hq, int(offs[j])) for j in range(wl.num_blocks) if offs[j + 1] > offs[j]]
+    must += [(0, (3 * j + 1) % wl.Hq, int(offs[j + 1]) - 1) for j in range(wl.num_blocks) if offs[j + 1] > offs[j]]
+    rows = gs.coverage_rows_prefill(np.random.default_rng(5), wl.B, wl.Hq, wl.Lq, must=must)
+    _covered(wl, cache, rows)
 
 
 def test_config5_streams_full_size():
     wl = inputs.config(5)
     cache = gs.device_cache(wl, wl.cache_lens, fill_on_gpu=True)
-    must = [(0, 0, 0), (3, 63, 511), (1, 8, 256), (2, 7, 255)]
-    _sampled(wl, cache, must=must, n=24)
+    rows = gs.coverage_rows_step(np.random.default_rng(5), wl.B, wl.Hq, wl.Hkv, wl.Lq,
+                                 must=[(3, 63, 511), (1, 8, 256), (2, 7, 255)])
+    _covered(wl, cache, rows)
     # the fused append committed the new block at positions 131072 ..
     kn = wl.k_new
     for b, t in [(0, 0), (3, 511), (2, 300)]:
@@ -172,11 +183,39 @@ def test_config5_streams_full_size():
 def test_long_streams_split_by_round_model_full_size():
     """3 streams of 512-token blocks over 131072 cached tokens (GQA 64/8):
     the 384 work-groups fill 1.5 rounds, so the planner splits the KV range
-    in two (workspace > 0); sampled rows of the first and last stream."""
+    in two (workspace > 0); one row of every packed 32-row block."""
     B = 3
     wl = inputs.step_workload(f"streams_b{B}_gqa64x8_d128_q512_c131072", B, 64, 8, 128, 512, [131072] * B,
                               seed=1020 + B, fuse_append=True)
-    assert ws.workspace_bytes(ws.WS_OP_STEP, B, 64, 8, 512, 131072 + 512) > 0
+    ns, need = ws.step_plan(B, 64, 8, 512, wl.cache_lens)
+    if torch.cuda.get_device_properties(0).multi_processor_count == 256:
+        assert ns == 2 and need > 0
     cache = gs.device_cache(wl, wl.cache_lens, fill_on_gpu=True)
-    _sampled(wl, cache, must=[(0, 0, 0), (B - 1, 63, 511), (B - 1, 5, 100)], n=16)
+    rows = gs.coverage_rows_step(np.random.default_rng(7), wl.B, wl.Hq, wl.Hkv, wl.Lq)
+    _covered(wl, cache, rows)
 
+
+def test_long_split_reads_page_ids_from_memory():
+    """One KV split longer than the page ids the kernel stages in LDS (2560
+    tiles = 163840 tokens): 170000 cached tokens in shuffled pages, one KV
+    head shared by 8 query heads, 4128 new tokens (33024 packed rows, 129
+    query tiles, so the plan uses one split); the pages past the staged ids
+    are looked up in the device page table.  One row of every packed 32-row
+    block (each sees every key)."""
+    wl = inputs.step_workload("step_long_split_b1_gqa8x1_q4128_c170000", 1, 8, 1, 128, 4128, [170000],
+                              seed=77, fuse_append=True)
+    ns, _ = ws.step_plan(1, 8, 1, 4128, wl.cache_lens)
+    if ns != 1:
+        pytest.skip(f"the device plan splits this step in {ns}")
+    assert (170000 + 63) // 64 > 2560
+    cache = gs.device_cache(wl, wl.cache_lens, fill_on_gpu=True)
+    rows = gs.coverage_rows_step(np.random.default_rng(8), wl.B, wl.Hq, wl.Hkv, wl.Lq, must=[(0, 7, 4127)])
+    _covered(wl, cache, rows)
+
+
+def test_device_plan_matches_its_compute_units():
+    """Steps are planned for the compute units the device reports."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    for args in ((1, 24, 24, 256, [4096]), (4, 64, 8, 16, [131072] * 4), (3, 64, 8, 512, [131072] * 3)):
+        assert ws.step_plan(*args) == ws.step_plan(*args, num_cus=cus)
+        assert ws.step_plan(*args)[1] == ws.workspace_bytes(ws.WS_OP_STEP, *args[:4], max(args[4]) + args[3])

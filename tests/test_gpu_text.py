@@ -147,14 +147,17 @@ def test_streaming_replay_equals_prefill_text():
 # full-size thinker workloads (sampled rows)
 
 def test_thinker_prefill_full_size():
+    """The thinker's pass at full size (128 interleaved units, GQA 40/8, each
+    unit's text segment token-causal): one row of every 32-row block of
+    every query head, plus each segment's first and last token."""
     wl = inputs.thinker_prefill()
     cache = gs.device_cache(wl, [wl.Lq], fill_on_gpu=True)
     ts, offs = wl.text_starts[0], wl.offsets[0]
-    must = [(0, 0, int(ts[j])) for j in (0, 60, 127)] + [(0, 39, int(offs[j + 1]) - 1) for j in (1, 64, 127)]
-    must += [(0, 7, int(ts[j]) - 1) for j in (3, 90) if ts[j] > offs[j]]
-    g = np.random.default_rng(5)
-    rows = inputs.sample_rows(g, wl.B, wl.Hq, wl.Lq, 40, must=must)
-    gs.say(f"[gpu] {wl.name}: full size, {len(rows)} sampled rows")
+    must = [(0, j % wl.Hq, int(ts[j])) for j in range(wl.num_blocks) if ts[j] < offs[j + 1]]
+    must += [(0, (5 * j + 2) % wl.Hq, int(offs[j + 1]) - 1) for j in range(wl.num_blocks)]
+    must += [(0, (7 * j + 3) % wl.Hq, int(ts[j]) - 1) for j in range(wl.num_blocks) if ts[j] > offs[j]]
+    rows = gs.coverage_rows_prefill(np.random.default_rng(5), wl.B, wl.Hq, wl.Lq, must=must)
+    gs.say(f"[gpu] {wl.name}: full size, {len(rows)} rows")
     out, lse = gs.run_gpu(wl, cache=cache)
     torch.cuda.synchronize()
     ref, ref_lse = gs.run_oracle(wl, rows=rows)
@@ -163,12 +166,13 @@ def test_thinker_prefill_full_size():
 
 
 def test_thinker_decode_step_full_size():
+    """The thinker's token-causal decode step at full size (4 streams x 8
+    tokens over 131072 cached tokens, GQA 64/8, KV splits): every output."""
     wl = inputs.thinker_step()
     cache = gs.device_cache(wl, wl.cache_lens, fill_on_gpu=True)
-    rows = [(b, h, t) for b in range(wl.B) for h in (0, 9, 63) for t in (0, 3, 7)]
-    gs.say(f"[gpu] {wl.name}: full size, {len(rows)} sampled rows")
+    gs.say(f"[gpu] {wl.name}: full size, every output")
     out, lse = gs.run_gpu(wl, cache=cache)
     torch.cuda.synchronize()
-    ref, ref_lse = gs.run_oracle(wl, rows=np.array(rows, np.int32))
-    gs.assert_close(gs.compare(out, lse, ref, ref_lse, rows=np.array(rows, np.int32)))
+    ref, ref_lse = gs.run_oracle(wl)
+    gs.assert_close(gs.compare(out, lse, ref, ref_lse))
     assert torch.isfinite(out).all()

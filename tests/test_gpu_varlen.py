@@ -178,8 +178,8 @@ def test_thinker_decode_varlen_full_size():
         wl.k[b, wl.Lc_max + int(n):] = float("nan")
         wl.v[b, wl.Lc_max + int(n):] = float("nan")
     cache = gs.device_cache(wl, wl.cache_lens, fill_on_gpu=True)
-    rows = _real_rows(wl, heads=(0, 9, 63))
-    gs.say(f"[gpu] {wl.name} varlen {wl.new_lens.tolist()}: full size, {len(rows)} sampled rows")
+    rows = _real_rows(wl, heads=range(wl.Hq))
+    gs.say(f"[gpu] {wl.name} varlen {wl.new_lens.tolist()}: full size, all {len(rows)} real rows")
     out, lse = gs.run_gpu(wl, cache=cache)
     torch.cuda.synchronize()
     ref, ref_lse = gs.run_oracle(wl, rows=rows)
@@ -212,8 +212,9 @@ def test_streams_varlen_full_size():
     for b in range(wl.B):
         n, ts = int(wl.new_lens[b]), int(wl.text_starts[b])
         must += [(b, 0, 0), (b, 63, n - 1), (b, 17, ts), (b, 40, max(ts - 1, 0))]
-    rows = inputs.sample_rows(np.random.default_rng(9), wl.B, wl.Hq, int(wl.new_lens.min()), 40, must=must)
-    gs.say(f"[gpu] {wl.name} new_lens {wl.new_lens.tolist()}: full size, {len(rows)} sampled rows")
+    rows = gs.coverage_rows_step(np.random.default_rng(9), wl.B, wl.Hq, wl.Hkv, wl.Lq, must=must,
+                                 new_lens=wl.new_lens)
+    gs.say(f"[gpu] {wl.name} new_lens {wl.new_lens.tolist()}: full size, {len(rows)} rows")
     out, lse = gs.run_gpu(wl, cache=cache)
     torch.cuda.synchronize()
     ref, ref_lse = gs.run_oracle(wl, rows=rows)
