@@ -55,7 +55,7 @@ def log(msg):
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    for p in ws._build.SOURCES:
+    for p in ws._build.KERNEL_SOURCES:
         h.update(open(p, "rb").read())
     return h.hexdigest()[:16]
 

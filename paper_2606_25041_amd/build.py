@@ -8,9 +8,12 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libwsattn.so")
-SOURCES = [os.path.join(CSRC, "ws_kernels.hip"), os.path.join(CSRC, "ws_api.cpp")]
+SOURCES = [os.path.join(CSRC, "ws_kernels.hip"), os.path.join(CSRC, "ws_api.cpp"),
+           os.path.join(CSRC, "ws_device.hip")]
 HEADERS = [os.path.join(CSRC, "ws_kernels.h"),
            os.path.join(os.path.dirname(HERE), "include", "ws_attn.h")]
+# the device code whose hash tags measured counter summaries
+KERNEL_SOURCES = [os.path.join(CSRC, "ws_kernels.hip"), os.path.join(CSRC, "ws_kernels.h")]
 ARCH = "gfx950"
 
 
@@ -42,11 +45,12 @@ def build(verbose=False):
     C ABI are compiled separately, then linked into one shared library."""
     common = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
               "-Wall", "-Wno-unused-function"]
-    kobj, aobj = LIB + ".kernels.o", LIB + ".api.o"
+    kobj, aobj, dobj = LIB + ".kernels.o", LIB + ".api.o", LIB + ".device.o"
     msgs = _run(common + KERNEL_FLAGS + ["-c", SOURCES[0], "-o", kobj])
     msgs += _run(common + ["-c", SOURCES[1], "-o", aobj])
-    msgs += _run([hipcc(), f"--offload-arch={ARCH}", "-shared", kobj, aobj, "-o", LIB + ".tmp"])
-    for f in (kobj, aobj):
+    msgs += _run(common + KERNEL_FLAGS + ["-c", SOURCES[2], "-o", dobj])
+    msgs += _run([hipcc(), f"--offload-arch={ARCH}", "-shared", kobj, aobj, dobj, "-o", LIB + ".tmp"])
+    for f in (kobj, aobj, dobj):
         os.remove(f)
     if verbose and msgs:
         print("\n".join(msgs))

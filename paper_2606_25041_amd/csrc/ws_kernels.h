@@ -2,6 +2,7 @@
 // (ws_api.cpp, no HIP headers) and the gfx950 kernels (ws_kernels.hip).
 #pragma once
 
+#include <stddef.h>
 #include <stdint.h>
 
 namespace ws {

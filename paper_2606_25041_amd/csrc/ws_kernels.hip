@@ -40,8 +40,6 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include <atomic>
-
 #include "ws_kernels.h"
 
 namespace ws {
@@ -100,9 +98,11 @@ __device__ __forceinline__ int row_key_end(const int32_t *off, const int32_t *te
     return text ? max(at(text, lo - 1), i + 1) : at(off, lo);
 }
 
+// Two floats rounded to bf16 (RNE), lo in the low half: one v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    __bf16 a = (__bf16)lo, b = (__bf16)hi;
-    return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 b16x2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, b16x2));
 }
 
 // s_waitcnt with vector-memory count <= N and LDS/scalar count = 0 (the export
@@ -1449,26 +1449,6 @@ int launch_append(const AppendArgs &a, void *stream) {
     if (gx < 1) gx = 1;
     hipLaunchKernelGGL(append_kernel, dim3((unsigned)gx, (unsigned)a.B), dim3(256), 0, st, a);
     return (int)hipGetLastError();
-}
-
-int current_device_cus(int *cus) {
-    constexpr int MAX_DEV = 64;
-    static std::atomic<int> cached[MAX_DEV];   // 0 until queried
-    int dev = -1;
-    if (hipError_t e = hipGetDevice(&dev)) return (int)e;
-    if (dev >= 0 && dev < MAX_DEV) {
-        const int c = cached[dev].load(std::memory_order_relaxed);
-        if (c > 0) {
-            *cus = c;
-            return 0;
-        }
-    }
-    int n = 0;
-    if (hipError_t e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev)) return (int)e;
-    if (n <= 0) return (int)hipErrorInvalidDevice;
-    if (dev >= 0 && dev < MAX_DEV) cached[dev].store(n, std::memory_order_relaxed);
-    *cus = n;
-    return 0;
 }
 
 int launch_prefill_bwd(const BwdArgs &a, int head_dim, void *stream) {

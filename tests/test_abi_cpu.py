@@ -394,6 +394,9 @@ def test_workspace_bytes(lib):
     # on a partition of 32 compute units the 24 tiles of the headline step
     # need fewer splits
     assert 1 < plan(lib, 32, 1, 24, 24, 256, [4096])[2] < plan(lib, 256, 1, 24, 24, 256, [4096])[2]
+    # 256 query tiles fill exactly one round of 256 CUs: one split (the GPU
+    # test of a split longer than the staged page ids relies on it)
+    assert plan(lib, 256, 1, 8, 1, 8192, [170000])[2] == 1
     assert lib.ws_workspace_bytes(ws.WS_OP_PREFILL, 2, 32, 8, 16384, 16384) == 0
     assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 0, 24, 24, 256, 4352) == 0
     assert lib.ws_workspace_bytes(ws.WS_OP_STEP, 1, 24, 5, 256, 4352) == 0   # 24 % 5 != 0
