@@ -208,6 +208,29 @@ int ws_block_causal_attn_fwd(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new,
                              void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * ws_block_causal_attn_fwd_noalloc -- ws_block_causal_attn_fwd for callers
+ * that cannot allocate device memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation.  It allocates nothing
+ * (no hipMalloc, hipFree or allocating library call): the split-KV partials
+ * go to a scratch array of WS_NOALLOC_SCRATCH_BYTES that the library's code
+ * object holds on each device (until the process ends) instead of a caller
+ * workspace.  Same arguments, results and errors as ws_block_causal_attn_fwd
+ * without workspace / workspace_bytes; a step whose plan needs more partial
+ * storage than the array holds (ws_step_plan reports it) gives
+ * WS_ERR_WORKSPACE.  Every call on a device shares that device's array and
+ * nothing in it needs to start at zero (each call writes the partials it
+ * reads); calls that may overlap on one device (unordered streams) race on
+ * it and give undefined results, so order them.
+ */
+#define WS_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+int ws_block_causal_attn_fwd_noalloc(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new,
+                                     const ws_paged_kv *kv,
+                                     const int32_t *cache_lens_host, const int32_t *cache_lens_dev,
+                                     int32_t batch, int32_t new_len, int32_t num_q_heads,
+                                     float scale, int32_t flags,
+                                     ws_tensor4 out, float *lse, void *stream);
+
+/*
  * ws_block_causal_prefill -- block-causal attention over whole sequences
  * (Sec. 2.4: the system prefill that builds the initial full-history state;
  * Sec. 2.3: training uses the same causal format as inference).

@@ -9,6 +9,7 @@ Entry points (same names as the C ABI, without the ``ws_`` prefix):
   kv_append(cache, cache_lens, k_new, v_new, new_lens=None)
   block_causal_attn_fwd(q, k_new, v_new, cache, cache_lens, ..., text_starts=None,
                         new_lens=None)
+  block_causal_attn_fwd_noalloc(q, k_new, v_new, cache, (lens_host, lens_dev), out, ...)
   block_causal_prefill(q, k, v, block_offsets, ..., text_starts=None)
 (with text_starts: the *_text entry points, blocks ending in a token-causal
 segment; with new_lens: the *_varlen entry points, new blocks of different
@@ -26,7 +27,7 @@ import torch  # loads the HIP runtime that libwsattn.so then shares
 
 from . import build as _build
 
-__all__ = ["WsError", "PagedCache", "kv_append", "block_causal_attn_fwd",
+__all__ = ["WsError", "PagedCache", "kv_append", "block_causal_attn_fwd", "block_causal_attn_fwd_noalloc",
            "block_causal_prefill", "block_causal_prefill_bwd", "workspace_bytes",
            "step_workspace_bytes_varlen", "step_plan", "library",
            "abi_version", "WS_OP_STEP", "WS_OP_PREFILL", "WS_OP_PREFILL_BWD", "PAGE_SIZE"]
@@ -35,6 +36,7 @@ WS_DTYPE_BF16, WS_DTYPE_F32 = 1, 2
 WS_FUSE_APPEND = 1
 WS_OP_STEP, WS_OP_PREFILL, WS_OP_PREFILL_BWD = 1, 2, 3
 PAGE_SIZE = 64
+NOALLOC_SCRATCH_BYTES = 32 << 20   # WS_NOALLOC_SCRATCH_BYTES of the C header
 STATUS = {0: "WS_OK", 1: "WS_ERR_NULL", 2: "WS_ERR_SHAPE", 3: "WS_ERR_UNSUPPORTED",
           4: "WS_ERR_ALIGN", 5: "WS_ERR_OFFSETS", 6: "WS_ERR_PAGE", 7: "WS_ERR_CAPACITY",
           8: "WS_ERR_HEADS", 9: "WS_ERR_WORKSPACE", 10: "WS_ERR_HIP"}
@@ -108,6 +110,10 @@ def library():
         lib.ws_block_causal_prefill_bwd.argtypes = [
             Tensor4, Tensor4, Tensor4, Tensor4, Tensor4, P, P, P, P, P, I32, I32, I32, I32, I32, I32, F,
             Tensor4, Tensor4, Tensor4, P, ctypes.c_size_t, P]
+        lib.ws_block_causal_attn_fwd_noalloc.restype = ctypes.c_int
+        lib.ws_block_causal_attn_fwd_noalloc.argtypes = [
+            Tensor4, Tensor4, Tensor4, ctypes.POINTER(PagedKVDesc), P, P, I32, I32, I32, F, I32,
+            Tensor4, P, P]
         lib.ws_step_plan.restype = ctypes.c_int
         lib.ws_step_plan.argtypes = [I32, I32, I32, I32, I32, P, P, ctypes.POINTER(I32),
                                      ctypes.POINTER(ctypes.c_size_t)]
@@ -328,6 +334,35 @@ def block_causal_attn_fwd(q, k_new, v_new, cache, cache_lens, scale=None, fuse_a
             th.data_ptr(), td.data_ptr(), B, Lq, Hq, float(scale), flags, _t4(out), _ptr(lse),
             ws_ptr, ws_len, _stream()))
     return (out, lse) if want_lse else out
+
+
+def block_causal_attn_fwd_noalloc(q, k_new, v_new, cache, cache_lens, out, lse=None, scale=None,
+                                  fuse_append=False):
+    """``block_causal_attn_fwd`` through the allocation-free entry point: the
+    split partials live in the library's per-device scratch array, and this
+    wrapper allocates nothing either, so every buffer comes from the caller:
+    cache_lens is a (host, device) pair of int32 [B] tensors, out the
+    [B][Lq][Hq][d] output (bf16 or f32), lse None or f32 [B][Hq][Lq].
+    Calls on one device must be ordered (they share the scratch array)."""
+    B, Lq, Hq, D = q.shape
+    if not isinstance(cache_lens, tuple):
+        raise ValueError("cache_lens must be a (host, device) pair of int32 tensors")
+    host, dev = cache_lens
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    _shape("k_new", k_new, (B, Lq, cache.num_kv_heads, D))
+    _shape("v_new", v_new, (B, Lq, cache.num_kv_heads, D))
+    _shape("out", out, (B, Lq, Hq, D))
+    _shape("lse", lse, (B, Hq, Lq))
+    if D != cache.head_dim:
+        raise ValueError("q head_dim differs from the cache's")
+    _check_lens(host, dev, B)
+    _check_table(cache, B)
+    desc = cache.desc()
+    _check(library().ws_block_causal_attn_fwd_noalloc(
+        _t4(q), _t4(k_new), _t4(v_new), ctypes.byref(desc), host.data_ptr(), dev.data_ptr(),
+        B, Lq, Hq, float(scale), WS_FUSE_APPEND if fuse_append else 0, _t4(out), _ptr(lse), _stream()))
+    return out
 
 
 def block_causal_prefill(q, k, v, block_offsets, scale=None, cache=None, num_kv_heads=None,

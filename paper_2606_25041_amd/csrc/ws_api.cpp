@@ -32,6 +32,7 @@ int ok() {
 }
 
 constexpr int WS_MAX_SPLITS = ws::MAX_SPLITS;
+static_assert(WS_NOALLOC_SCRATCH_BYTES == ws::NOALLOC_SCRATCH_BYTES, "one scratch size");
 // packed query rows of one (stream, KV head) in a step: G x new_len (the
 // kernels index them in 32-bit arithmetic)
 constexpr int64_t WS_MAX_STEP_ROWS = ((int64_t)1 << 30);
@@ -242,7 +243,7 @@ int step_impl(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_k
               const int32_t *text_host, const int32_t *text_dev, int32_t batch,
               int32_t new_len, int32_t num_q_heads, float scale, int32_t flags,
               ws_tensor4 out, float *lse, void *workspace, size_t workspace_bytes,
-              void *stream);
+              void *stream, bool noalloc = false);
 int append_impl(const ws_paged_kv *kv, int32_t batch, const int32_t *cache_lens_host,
                 const int32_t *cache_lens_dev, const int32_t *nl_host, const int32_t *nl_dev, int32_t new_len,
                 ws_tensor4 k_new, ws_tensor4 v_new, void *stream);
@@ -366,6 +367,14 @@ int ws_block_causal_attn_fwd(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, c
                              void *stream) {
     return step_impl(q, k_new, v_new, kv, cache_lens_host, cache_lens_dev, nullptr, nullptr, nullptr, nullptr, batch,
                      new_len, num_q_heads, scale, flags, out, lse, workspace, workspace_bytes, stream);
+}
+
+int ws_block_causal_attn_fwd_noalloc(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_kv *kv,
+                                     const int32_t *cache_lens_host, const int32_t *cache_lens_dev, int32_t batch,
+                                     int32_t new_len, int32_t num_q_heads, float scale, int32_t flags,
+                                     ws_tensor4 out, float *lse, void *stream) {
+    return step_impl(q, k_new, v_new, kv, cache_lens_host, cache_lens_dev, nullptr, nullptr, nullptr, nullptr, batch,
+                     new_len, num_q_heads, scale, flags, out, lse, nullptr, 0, stream, true);
 }
 
 int ws_block_causal_attn_fwd_text(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_kv *kv,
@@ -535,7 +544,7 @@ int step_impl(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_k
               const int32_t *text_host, const int32_t *text_dev, int32_t batch,
               int32_t new_len, int32_t num_q_heads, float scale, int32_t flags,
               ws_tensor4 out, float *lse, void *workspace, size_t workspace_bytes,
-              void *stream) {
+              void *stream, bool noalloc) {
     if (int rc = check_paged(kv)) return rc;
     if (!cache_lens_host || !cache_lens_dev) return fail(WS_ERR_NULL, "cache_lens pointer is NULL");
     if (batch < 0 || new_len < 0 || num_q_heads <= 0)
@@ -575,6 +584,21 @@ int step_impl(ws_tensor4 q, ws_tensor4 k_new, ws_tensor4 v_new, const ws_paged_k
         return fail(WS_ERR_HIP, "cannot query the device's compute units (hip error %d)", e);
     const StepPlan plan = plan_step(cus, batch, num_q_heads, kv->num_kv_heads, new_len, max_k, nl_host);
     const size_t need_ws = step_workspace(plan, batch, num_q_heads, kv->num_kv_heads, new_len);
+    if (noalloc) {
+        // the library's per-device scratch array stands in for the workspace
+        if (need_ws > ws::NOALLOC_SCRATCH_BYTES)
+            return fail(WS_ERR_WORKSPACE,
+                        "this step needs %zu bytes of split partials; the allocation-free entry point "
+                        "holds at most %zu (use ws_block_causal_attn_fwd with a workspace)",
+                        need_ws, ws::NOALLOC_SCRATCH_BYTES);
+        workspace = nullptr;
+        workspace_bytes = 0;
+        if (need_ws > 0) {
+            if (int e = ws::scratch_address(&workspace))
+                return fail(WS_ERR_HIP, "cannot look up the scratch array's device address (hip error %d)", e);
+            workspace_bytes = ws::NOALLOC_SCRATCH_BYTES;
+        }
+    }
     if (need_ws > 0 && (!workspace || workspace_bytes < need_ws || !aligned16(workspace)))
         return fail(WS_ERR_WORKSPACE, "workspace needs %zu bytes (16-byte aligned), got %zu", need_ws,
                     workspace ? workspace_bytes : (size_t)0);

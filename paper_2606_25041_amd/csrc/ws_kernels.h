@@ -167,4 +167,10 @@ int launch_prefill_bwd(const BwdArgs &a, int head_dim, void *stream);
 // cached): 0 and *cus set, or a HIP error code (e.g. no device).
 int current_device_cus(int *cus);
 
+// Bytes of the per-device scratch array behind the allocation-free step.
+constexpr size_t NOALLOC_SCRATCH_BYTES = (size_t)32 << 20;
+// Device address of the current device's scratch array (looked up once per
+// device): 0 and *ptr set, or a HIP error code.
+int scratch_address(void **ptr);
+
 }  // namespace ws

@@ -43,7 +43,8 @@ def test_exports_every_declared_symbol(lib):
     assert {"ws_kv_append", "ws_block_causal_attn_fwd", "ws_block_causal_prefill",
             "ws_block_causal_attn_fwd_text", "ws_block_causal_prefill_text", "ws_block_causal_prefill_bwd",
             "ws_block_causal_attn_fwd_varlen", "ws_kv_append_varlen", "ws_step_workspace_bytes_varlen",
-            "ws_workspace_bytes", "ws_step_plan", "ws_abi_version", "ws_status_string",
+            "ws_workspace_bytes", "ws_step_plan", "ws_block_causal_attn_fwd_noalloc", "ws_abi_version",
+            "ws_status_string",
             "ws_last_error"} <= set(names)
     for name in names:
         assert hasattr(lib, name), name
@@ -142,6 +143,26 @@ def test_step_errors(lib):
     assert plan(lib, 256, 2, 4, 2, 16, [10, 200])[1] > 0
     assert step_call(lib, hw, wsp=None) == 10
     assert b"compute units" in lib.ws_last_error()
+
+
+def test_step_noalloc_validates_like_the_workspace_entry_point(lib):
+    h = Host()
+
+    def call(q=None, B=2, Lq=16, Hq=4, flags=0, lse=None, lens_ptr="host"):
+        desc = h.desc()
+        lh = h.lens.ctypes.data if lens_ptr == "host" else lens_ptr
+        return lib.ws_block_causal_attn_fwd_noalloc(q or t4(H=Hq, L=Lq), t4(H=2, L=Lq), t4(H=2, L=Lq),
+                                                    ctypes.byref(desc), lh, FAKE, B, Lq, Hq, 0.088, flags,
+                                                    t4(H=Hq, L=Lq), lse, None)
+    assert call(q=t4(ptr=None)) == 1
+    assert call(lens_ptr=None) == 1
+    assert call(B=-1) == 2
+    assert call(flags=4) == 3
+    assert call(lse=FAKE + 2) == 4
+    assert call(Hq=3) == 8
+    assert call(B=0) == 0                      # nothing to do
+    # valid arguments reach the device plan (no device here)
+    assert call() == 10
 
 
 def test_step_capacity_counts_fused_append(lib):
