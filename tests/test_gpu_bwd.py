@@ -11,6 +11,7 @@ import torch
 
 import oracle
 import paper_2606_25041_amd as ws
+from oracle import bwd_blocks
 from paper_2606_25041_amd import inputs
 from tests import gpu_support as gs
 
@@ -115,3 +116,56 @@ def test_bwd_full_size_prefill_closed_form():
     rhs = do64.sum(dim=(1, 3))
     bound = (2.0 ** -9 + 1e-5) * do64.abs().sum(dim=(1, 3)) + 1e-3
     assert bool(((lhs - rhs).abs() <= bound).all()), float(((lhs - rhs).abs() - bound).max())
+
+
+def _compare(name, got, ref):
+    assert np.all(np.isfinite(got)), name
+    err = np.abs(got - ref)
+    gs.say(f"[gpu]   {name}: {err.size} elements, max {err.max():.2e} mean {err.mean():.2e}")
+    assert err.max() <= gs.MAX_ABS and err.mean() <= gs.MEAN_ABS, (name, err.max(), err.mean())
+
+
+def test_bwd_full_size_elementwise():
+    """The whole-sequence workload (2 x 16384 tokens, GQA 32/8, 64 blocks of
+    256) at full size, element by element against the block-wise fp64
+    oracle: every dQ, dK and dV of one KV group per stream; for every other
+    group, the dK, dV of the keys of the last block and the dQ of its
+    queries (the last block's keys are seen by its own queries only); and
+    one dQ row of every (stream, query head, 128-row tile), its 32-row wave
+    and lane rotating with the tile."""
+    wl = inputs.config(3)
+    dout = inputs.bf16_normal(inputs.rng(93, 9), tuple(wl.q.shape))
+    q, k, v = gs.to_dev_bf16(wl.q), gs.to_dev_bf16(wl.k), gs.to_dev_bf16(wl.v)
+    gs.say("[gpu] bwd full-size prefill, element-wise")
+    o, lse = ws.block_causal_prefill(q, k, v, wl.offsets, want_lse=True)
+    dq, dk, dv = ws.block_causal_prefill_bwd(q, k, v, o, gs.to_dev_bf16(dout), lse, wl.offsets)
+    torch.cuda.synchronize()
+    B, L, Hq, Hkv = wl.B, wl.Lq, wl.Hq, wl.Hkv
+    G = Hq // Hkv
+    nb = wl.offsets.shape[1] - 1
+    bits = [inputs.bf16_bits(x) for x in (wl.q, wl.k, wl.v, dout)]
+    full = {(0, 0), (B - 1, Hkv - 1)}
+    got, ref = {"dq": [], "dk": [], "dv": []}, {"dq": [], "dk": [], "dv": []}
+    for b in range(B):
+        for g in range(Hkv):
+            n0 = 0 if (b, g) in full else nb - 1
+            lo = int(wl.offsets[b, n0])
+            r = bwd_blocks.prefill_bwd_group(*bits, wl.offsets, wl.scale, b, g, n0)
+            x = (dq[b, lo:, g * G:(g + 1) * G], dk[b, lo:, g], dv[b, lo:, g])
+            for name, gx, rx in zip(("dq", "dk", "dv"), x, r):
+                got[name].append(gx.float().cpu().numpy().astype(np.float64).ravel())
+                ref[name].append(rx.ravel())
+    for name in ("dq", "dk", "dv"):
+        _compare(name, np.concatenate(got[name]), np.concatenate(ref[name]))
+    rows = []
+    for b in range(B):
+        for h in range(Hq):
+            for t in range((L + 127) // 128):
+                i = 128 * t + 32 * ((t + h) % 4) + (7 * t + 3 * h + 11 * b) % 32
+                if i < L:
+                    rows.append((b, h, i))
+    rows = np.asarray(rows)
+    want = bwd_blocks.prefill_dq_rows(*bits, wl.offsets, wl.scale, rows)
+    idx = torch.from_numpy(rows).to(dq.device)
+    sel = dq[idx[:, 0], idx[:, 2], idx[:, 1]].float().cpu().numpy().astype(np.float64)
+    _compare("dq rows", sel, want)
