@@ -1060,7 +1060,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const BwdArgs a) {
 }
 
 // Loads rows [r0, r0 + nrows) of a [rows][D] bf16 tile (row r of the tile
-// = global row min(r0 + r, rmax)) straight into LDS at `lds` in the
+// = global row min(r0 + r, rmax), at least 0) straight into LDS at `lds` in the
 // swizzled layout, spread over NWV waves: wave-wide load i of wave w fills
 // tile bytes [(i * NWV + w) * 1024, +1024), lane l the 16 bytes at +16 l,
 // so it fetches the chunk that belongs there.  The caller waits for them
@@ -1075,16 +1075,18 @@ __device__ __forceinline__ void dma_rows(const char *g, int64_t st_bytes, int r0
     for (int i = 0; i < NI; ++i) {
         const int r = (i * NWV + wave) * RPW + lane / LPR;
         const int ch = (lane % LPR) ^ swz<D>(r);
-        const int gr = min(r0 + r, rmax);
+        const int gr = max(min(r0 + r, rmax), 0);
         dma16(g + (int64_t)gr * st_bytes + 16 * ch, lds + (i * NWV + wave) * 1024);
     }
 }
 
 // dQ: one work-group = (stream, query head, 128 query rows), 4 waves x 32
 // rows; K/V tiles of 64 keys go straight to LDS (two stages); tiles past
-// the last row's key end are never loaded.
+// the last row's key end are never loaded.  Registers are held to two waves
+// per SIMD, so two work-groups share a CU and one's softmax arithmetic runs
+// beside the other's MFMAs.
 template <int D>
-__global__ __launch_bounds__(256) void bwd_dq_kernel(const BwdArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void bwd_dq_kernel(const BwdArgs a) {
     constexpr int ROWB = 2 * D, KK = D / 16, MD = D / 32;
     constexpr int TILEB = 64 * ROWB;
     __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * TILEB];   // [stage][K, V]
@@ -1143,39 +1145,39 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(const BwdArgs a) {
         // the other stage was last read before the previous barrier
         if (t + 1 < ntile) issue_tile(t + 1);
         const char *kt = smem + (t & 1) * 2 * TILEB, *vt = kt + TILEB;
-        f32x16 S[2], dPt[2];
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) S[mb][v] = dPt[mb][v] = 0.f;
-        // S^T = K Q^T and dP^T = V dO^T (keys as rows)
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk)
-#pragma unroll
-            for (int mb = 0; mb < 2; ++mb) {
-                const bf16x8 ka = *(const bf16x8 *)(kt + mb * 32 * ROWB + (kbase ^ (32 * kk)));
-                S[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[kk], S[mb], 0, 0, 0);
-                const bf16x8 va = *(const bf16x8 *)(vt + mb * 32 * ROWB + (kbase ^ (32 * kk)));
-                dPt[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, dof[kk], dPt[mb], 0, 0, 0);
-            }
-        // dS^T = P^T (dP^T - D), rounded to bf16 as B fragments
         const bool need_mask = (t + 1) * 64 > kfull;
-        bf16x8 dsf[4];
+        // one half of the tile (32 keys) at a time, so that S^T and dP^T of
+        // a half, not of the whole tile, are live
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
+        for (int mb = 0; mb < 2; ++mb) {
+            // S^T = K Q^T and dP^T = V dO^T (keys as rows)
+            f32x16 S, dPt;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) S[v] = dPt[v] = 0.f;
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                const bf16x8 ka = *(const bf16x8 *)(kt + mb * 32 * ROWB + (kbase ^ (32 * kk)));
+                S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[kk], S, 0, 0, 0);
+                const bf16x8 va = *(const bf16x8 *)(vt + mb * 32 * ROWB + (kbase ^ (32 * kk)));
+                dPt = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, dof[kk], dPt, 0, 0, 0);
+            }
+            // dS^T = P^T (dP^T - D), rounded to bf16 as B fragments
+            bf16x8 dsf[2];
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int key = t * 64 + mb * 32 + 8 * (v >> 2) + 4 * hf + (v & 3);
-                const float p0 = fast_exp2(__builtin_fmaf(S[mb][v], c2, -lse2));
+                const float p0 = fast_exp2(__builtin_fmaf(S[v], c2, -lse2));
                 const float p = (!need_mask || key < my_kend) ? p0 : 0.f;
-                dsf[(16 * mb + v) >> 3][v & 7] = (__bf16)(p * (dPt[mb][v] - Dr));
+                dsf[v >> 3][v & 7] = (__bf16)(p * (dPt[v] - Dr));
             }
-        // dQ^T += K^T dS^T
+            // dQ^T += K^T dS^T over this half's keys
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
+            for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
-            for (int md = 0; md < MD; ++md)
-                acc[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<D>(kt, tb, ks, md), dsf[ks], acc[md], 0, 0, 0);
+                for (int md = 0; md < MD; ++md)
+                    acc[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<D>(kt, tb, 2 * mb + k2, md), dsf[k2],
+                                                                     acc[md], 0, 0, 0);
+        }
         wait_vm_lgkm<0>();   // tile t + 1 landed (and this tile's LDS reads are done)
         wg_barrier();
     }
@@ -1195,10 +1197,10 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(const BwdArgs a) {
 
 // dK and dV: one work-group = (stream, KV head, 128 keys), 8 waves: wave w
 // owns keys 32 (w % 4) .. + 31 and belongs to group w / 4.  The
-// work-group's K and V stay in LDS; the chunks of 32 query rows (from the
-// first row that sees any of these keys, for every query head of the KV
-// group) alternate between the two groups, each with its own two LDS
-// stages, so two waves share every SIMD.  At the end group 1 hands its
+// work-group's K and V stay in LDS; the chunks of 32 query rows (every row
+// that sees any of these keys, for every query head of the KV group, walked
+// from the sequence end) alternate between the two groups, each with its own
+// two LDS stages, so two waves share every SIMD.  At the end group 1 hands its
 // partial sums to group 0 through LDS (fixed order: group 0's + group 1's).
 template <int D>
 __global__ __launch_bounds__(512) void bwd_dkdv_kernel(const BwdArgs a) {
@@ -1242,6 +1244,12 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(const BwdArgs a) {
         if (ld_uniform(kend_b, mid) > kw0) hi = mid; else lo = mid + 1;
     }
     const int i0 = lo;
+    // Chunks of 32 query rows counted from the sequence end, down to row i0,
+    // with the query heads innermost: chunk it holds rows L - 32 (c + 1) ..
+    // L - 32 c - 1 (c = it / G) of head it % G.  The work-groups of a KV head
+    // (different key tiles, running side by side) then read the same rows at
+    // about the same time and the L2 serves them once.  Rows before i0 see
+    // none of these keys, so the masking zeroes their terms.
     const int nch = (a.L - i0 + 31) / 32;
     const int total = a.G * nch;            // chunks; group grp takes chunks grp, grp + 2, ...
     const int nstep = (total + 1) / 2;
@@ -1252,16 +1260,16 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(const BwdArgs a) {
     // the DMA of chunk it (Q and dO rows) and the (lse2, D, key end) of its
     // rows into registers; group-uniform
     auto issue_chunk = [&](int it) {
-        const int hh = it / nch, ch = it - hh * nch;
+        const int c = it / a.G, hh = it - c * a.G;
         const int h = kvh * a.G + hh;
-        const int r0 = i0 + 32 * ch;
+        const int r0 = a.L - 32 * (c + 1);   // may be negative: such rows are no rows
         const uint32_t base = lds_addr(smem) + chunk_base(it);
         dma_rows<D, 4, 32>((const char *)(a.q + b * a.q_sb + h * a.q_sh), 2 * a.q_st, r0, a.L - 1, base, sub, lane);
         dma_rows<D, 4, 32>((const char *)(a.dout + b * a.do_sb + h * a.do_sh), 2 * a.do_st, r0, a.L - 1,
                            base + TILEC, sub, lane);
         if (gtid < 32) {
             const int r = r0 + gtid;
-            if (r < a.L) {
+            if (r >= 0) {
                 const int64_t idx = ((int64_t)b * a.Hq + h) * a.L + r;
                 lreg = a.dl[2 * idx];
                 dreg = a.dl[2 * idx + 1];
