@@ -8,12 +8,19 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libwsattn.so")
-SOURCES = [os.path.join(CSRC, "ws_kernels.hip"), os.path.join(CSRC, "ws_api.cpp"),
-           os.path.join(CSRC, "ws_device.hip")]
-HEADERS = [os.path.join(CSRC, "ws_kernels.h"),
+# device sources (built with KERNEL_FLAGS) and the host-only C ABI
+DEVICE_SOURCES = [os.path.join(CSRC, "ws_kernels.hip"), os.path.join(CSRC, "ws_bwd.hip"),
+                  os.path.join(CSRC, "ws_device.hip")]
+HOST_SOURCES = [os.path.join(CSRC, "ws_api.cpp")]
+SOURCES = DEVICE_SOURCES + HOST_SOURCES
+HEADERS = [os.path.join(CSRC, "ws_kernels.h"), os.path.join(CSRC, "ws_device_util.h"),
            os.path.join(os.path.dirname(HERE), "include", "ws_attn.h")]
-# the device code whose hash tags measured counter summaries
-KERNEL_SOURCES = [os.path.join(CSRC, "ws_kernels.hip"), os.path.join(CSRC, "ws_kernels.h")]
+# the device code whose hash tags measured counter summaries: the forward
+# kernels (attention, merge, append) and, separately, the gradient kernels
+KERNEL_SOURCES = [os.path.join(CSRC, "ws_kernels.hip"), os.path.join(CSRC, "ws_kernels.h"),
+                  os.path.join(CSRC, "ws_device_util.h")]
+BWD_KERNEL_SOURCES = [os.path.join(CSRC, "ws_bwd.hip"), os.path.join(CSRC, "ws_kernels.h"),
+                      os.path.join(CSRC, "ws_device_util.h")]
 ARCH = "gfx950"
 
 
@@ -45,12 +52,14 @@ def build(verbose=False):
     C ABI are compiled separately, then linked into one shared library."""
     common = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
               "-Wall", "-Wno-unused-function"]
-    kobj, aobj, dobj = LIB + ".kernels.o", LIB + ".api.o", LIB + ".device.o"
-    msgs = _run(common + KERNEL_FLAGS + ["-c", SOURCES[0], "-o", kobj])
-    msgs += _run(common + ["-c", SOURCES[1], "-o", aobj])
-    msgs += _run(common + KERNEL_FLAGS + ["-c", SOURCES[2], "-o", dobj])
-    msgs += _run([hipcc(), f"--offload-arch={ARCH}", "-shared", kobj, aobj, dobj, "-o", LIB + ".tmp"])
-    for f in (kobj, aobj, dobj):
+    objs, msgs = [], []
+    for src in SOURCES:
+        obj = LIB + "." + os.path.splitext(os.path.basename(src))[0] + ".o"
+        flags = KERNEL_FLAGS if src in DEVICE_SOURCES else []
+        msgs += _run(common + flags + ["-c", src, "-o", obj])
+        objs.append(obj)
+    msgs += _run([hipcc(), f"--offload-arch={ARCH}", "-shared"] + objs + ["-o", LIB + ".tmp"])
+    for f in objs:
         os.remove(f)
     if verbose and msgs:
         print("\n".join(msgs))

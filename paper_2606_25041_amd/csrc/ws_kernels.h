@@ -1,5 +1,6 @@
 // Internal interface between the host-side validation/planning code
-// (ws_api.cpp, no HIP headers) and the gfx950 kernels (ws_kernels.hip).
+// (ws_api.cpp, no HIP headers) and the gfx950 kernels (ws_kernels.hip for
+// attention, merge and append; ws_bwd.hip for the gradients).
 #pragma once
 
 #include <stddef.h>
