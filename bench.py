@@ -190,13 +190,15 @@ class DeviceCase:
                                     lse=self.lse, want_lse=True, text_starts=self.text)
 
 
-def time_workload(wl, steps, warmup, dev, rotate=True, latency_steps=None, stats=None):
+def time_workload(wl, steps, warmup, dev, rotate=True, latency_steps=None, stats=None, graph_stats=None):
     """Returns (ms per step from the synchronised wall clock over the K timed
     steps, ms per step from HIP events recorded on the launch stream at the
     two ends of the same timed region, median per-step latency in ms, one
     case).  The timed region has no per-step instrumentation; the per-step
     latency comes from a separate loop afterwards, each step between two
-    events."""
+    events.  graph_stats (a dict): also the per-step latency with each step
+    (fused append, attention and merge) launched from a captured HIP graph,
+    median / p10 / p90 in ms."""
     nbytes = algorithmic_bytes(wl)
     copies = max(1, math.ceil(ROTATE_BYTES / nbytes)) if rotate else 1
     copies = min(copies, 16)
@@ -229,7 +231,42 @@ def time_workload(wl, steps, warmup, dev, rotate=True, latency_steps=None, stats
         stats["p90"] = float(np.percentile(lats, 90)) if n_lat else ev_ms
     log(f"[bench] {wl.name}: wall {wall_ms:.4f} ms/step, events over the timed region {ev_ms:.4f} "
         f"ms/step, per-step latency median {lat:.4f} ms")
+    if graph_stats is not None and n_lat:
+        graph_latency(cases, n_lat, graph_stats)
+        log(f"[bench] {wl.name}: per-step latency from HIP graph launches, median {graph_stats['median']:.4f} ms")
     return wall_ms, ev_ms, lat, cases[0]
+
+
+def graph_latency(cases, n, stats):
+    """Each case's step captured once into a HIP graph (after a warm-up on a
+    side stream); then n graph launches, each between two events."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for c in cases:
+            c.run()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graphs = []
+    for c in cases:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            c.run()
+        graphs.append(g)
+    for g in graphs:
+        g.replay()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    for i in range(n):
+        ev[i][0].record()
+        graphs[i % len(graphs)].replay()
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    lats = [a.elapsed_time(b) for a, b in ev]
+    stats["median"] = float(np.median(lats))
+    stats["p10"] = float(np.percentile(lats, 10))
+    stats["p90"] = float(np.percentile(lats, 90))
+    del graphs
 
 
 # ---------------------------------------------------------------------------
@@ -486,7 +523,19 @@ def oracle_sample(wl, seed=11):
     dt = time.perf_counter() - t0
     log(f"[bench] oracle {wl.name}: {dt:.2f} s for {pairs:.3g} pairs")
     return {"workload": wl.name, "value": 4.0 * wl.D * pairs / dt / 1e12, "unit": "TFLOP/s", "cores": threads,
-            "kind": "oracle", "seconds": round(dt, 3), "sample": sample}
+            "kind": "oracle", "seconds": round(dt, 3), "sample": sample, "cpu_model": cpu_model()}
+
+
+def cpu_model():
+    """The host CPU's model name (Linux /proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def replay_timing(idx, dev, reps=5):
@@ -737,8 +786,9 @@ def main():
     wl = workload(args.config)
     flops, nbytes = algorithmic_flops(wl), algorithmic_bytes(wl)
     torch.cuda.synchronize()
-    lat_stats = {}
-    wall_ms, ev_mean, ev_med, _ = time_workload(wl, args.steps, args.warmup, dev, stats=lat_stats)
+    lat_stats, graph_stats = {}, {}
+    wall_ms, ev_mean, ev_med, _ = time_workload(wl, args.steps, args.warmup, dev, stats=lat_stats,
+                                                graph_stats=graph_stats if wl.kind == "step" else None)
     tflops = flops / (wall_ms * 1e-3) / 1e12
     roof = roofline_of(wl, ev_mean, flops, nbytes)
 
@@ -752,13 +802,16 @@ def main():
             # interleaved unit of its own length in one step
             w2 = (inputs.thinker_prefill() if idx == "thinker" else inputs.streams_varlen() if idx == "varlen"
                   else workload(idx))
-            st = {}
+            st, gst = {}, {}
             n_steps = args.steps if w2.kind == "step" and idx == 2 else max(3, args.steps // 5)
             wms, emean, emed, _ = time_workload(w2, n_steps, 2, dev, latency_steps=n_steps if idx == 2 else 0,
-                                                stats=st if idx == 2 else None)
+                                                stats=st if idx == 2 else None,
+                                                graph_stats=gst if idx == 2 else None)
             rec = step_record(w2, wms, emean, emed, st if idx == 2 else None)
             if idx == 2:   # the single-block step: HBM-bound, reported with its roofline
                 rec["roofline"] = roofline_of(w2, emean, algorithmic_flops(w2), algorithmic_bytes(w2))
+                rec["latency_ms_per_block_graph"] = round(gst["median"], 5)
+                rec["latency_ms_p10_p90_graph"] = [round(gst["p10"], 5), round(gst["p90"], 5)]
             extra.append(rec)
             del w2
             torch.cuda.empty_cache()
@@ -776,6 +829,9 @@ def main():
             if r2:
                 r2["frac_of_measured_ceiling"] = round(r2["achieved"] / (
                     ceil["mfma_bf16_TFLOP/s"] if r2["bound"] == "mfma" else ceil["hbm_read_GB/s"]), 4)
+        for pt in sweeps:   # the binding roof rebuilt from the two measured ceilings
+            attain = min(ceil["mfma_bf16_TFLOP/s"], pt["flop_per_byte"] * ceil["hbm_read_GB/s"] / 1e3)
+            pt["frac_of_measured_bound"] = round(pt["TFLOP/s"] / attain, 4)
     cpu = None
     if not args.no_cpu:
         cpu = oracle_sample(wl)
@@ -804,6 +860,9 @@ def main():
                    "parallelism": "none (1 GPU)"},
         "latency_ms_per_block": round(ev_med, 5),
         "latency_ms_p10_p90": [round(lat_stats["p10"], 5), round(lat_stats["p90"], 5)],
+        "latency_ms_per_block_graph": round(graph_stats["median"], 5) if graph_stats else None,
+        "latency_ms_p10_p90_graph": ([round(graph_stats["p10"], 5), round(graph_stats["p90"], 5)]
+                                     if graph_stats else None),
         "roofline": roof,
         "cpu_baseline": cpu,
         "ceilings": ceil,
