@@ -115,6 +115,36 @@ def compare(out, lse, ref_out, ref_lse, rows=None):
     return stats
 
 
+def run_block_oracle(wl, groups=None):
+    """Every output and lse of a workload from the block-wise fp64 oracle
+    (``oracle.blocks``, pinned to the loop oracle): float64 numpy (out, lse);
+    groups: optional (b, KV head) list to compute, the rest NaN (as are a
+    step's padding rows)."""
+    from oracle import blocks
+    bits = inputs.bf16_bits
+    if wl.kind == "step":
+        return blocks.step(bits(wl.q), bits(wl.k_cache), bits(wl.v_cache), wl.cache_lens, bits(wl.k_new),
+                           bits(wl.v_new), wl.scale, text_starts=wl.text_starts,
+                           new_lens=getattr(wl, "new_lens", None), groups=groups)
+    return blocks.prefill(bits(wl.q), bits(wl.k), bits(wl.v), wl.offsets, wl.scale,
+                          text_starts=wl.text_starts, groups=groups)
+
+
+def compare_all(out, lse, ref_out, ref_lse):
+    """Element-wise errors over every output (and lse) the oracle computed
+    (entries it left NaN are skipped)."""
+    o = out.detach().to(torch.float64).cpu().numpy()
+    sel = ~np.isnan(ref_out)
+    err = np.abs(o[sel] - ref_out[sel])
+    stats = {"elements": int(sel.sum()), "max_abs": float(err.max()), "mean_abs": float(err.mean()),
+             "finite": bool(np.all(np.isfinite(o)))}
+    if lse is not None:
+        l = lse.detach().to(torch.float64).cpu().numpy()
+        ls = ~np.isnan(ref_lse)
+        stats["lse_max_abs"] = float(np.abs(l[ls] - ref_lse[ls]).max())
+    return stats
+
+
 def assert_close(stats):
     assert stats["finite"], stats
     assert stats["max_abs"] <= MAX_ABS, stats

@@ -11,7 +11,7 @@ import torch
 
 import oracle
 import paper_2606_25041_amd as ws
-from oracle import bwd_blocks
+from oracle import blocks
 from paper_2606_25041_amd import inputs
 from tests import gpu_support as gs
 
@@ -150,7 +150,7 @@ def test_bwd_full_size_elementwise():
         for g in range(Hkv):
             n0 = 0 if (b, g) in full else nb - 1
             lo = int(wl.offsets[b, n0])
-            r = bwd_blocks.prefill_bwd_group(*bits, wl.offsets, wl.scale, b, g, n0)
+            r = blocks.prefill_bwd_group(*bits, wl.offsets, wl.scale, b, g, n0)
             x = (dq[b, lo:, g * G:(g + 1) * G], dk[b, lo:, g], dv[b, lo:, g])
             for name, gx, rx in zip(("dq", "dk", "dv"), x, r):
                 got[name].append(gx.float().cpu().numpy().astype(np.float64).ravel())
@@ -165,7 +165,7 @@ def test_bwd_full_size_elementwise():
                 if i < L:
                     rows.append((b, h, i))
     rows = np.asarray(rows)
-    want = bwd_blocks.prefill_dq_rows(*bits, wl.offsets, wl.scale, rows)
+    want = blocks.prefill_dq_rows(*bits, wl.offsets, wl.scale, rows)
     idx = torch.from_numpy(rows).to(dq.device)
     sel = dq[idx[:, 0], idx[:, 2], idx[:, 1]].float().cpu().numpy().astype(np.float64)
     _compare("dq rows", sel, want)

@@ -1,7 +1,9 @@
 """GPU parity: the HIP path (through the C ABI) against the fp64 oracle,
 element by element on seeded inputs.  Small cases span several 64-key tiles,
 several query tiles and ragged tails; the five named workloads run at full
-size and are checked on sampled rows that the oracle computes one by one.
+size and are checked on sampled rows that the loop oracle computes one by
+one (one in every 32-row block of every work item) and, for the larger ones,
+on every output against the block-wise fp64 oracle.
 Tolerance: max-abs 2e-2, mean-abs 2e-3 (bf16 outputs), lse 1e-3."""
 import numpy as np
 import pytest
@@ -178,6 +180,36 @@ def test_config5_streams_full_size():
         page = int(wl.page_table[b][pos // 64])
         got = cache.k_pool[page, :, pos % 64].cpu()
         assert torch.equal(got.view(torch.int16), kn[b, t].view(torch.int16))
+
+
+def _every_output(wl, cache=None, groups=None):
+    """Full-size run against the block-wise fp64 oracle on every output
+    element and lse (of the given (stream, KV head) groups, if any)."""
+    gs.say(f"[gpu] {wl.name}: full size, every output" + (f" of groups {groups}" if groups else ""))
+    out, lse = gs.run_gpu(wl, cache=cache)
+    torch.cuda.synchronize()
+    ref, ref_lse = gs.run_block_oracle(wl, groups=groups)
+    stats = gs.compare_all(out, lse, ref, ref_lse)
+    gs.say(f"[gpu]   {stats}")
+    gs.assert_close(stats)
+    assert torch.isfinite(out).all()
+
+
+def test_config3_prefill_every_output():
+    _every_output(inputs.config(3))
+
+
+def test_config4_interleaved_every_output():
+    wl = inputs.config(4)
+    _every_output(wl, cache=gs.device_cache(wl, [wl.Lq], fill_on_gpu=True))
+
+
+def test_config5_streams_every_output_of_four_groups():
+    """Every output of one KV group per stream (KV heads 0, 3, 5, 7: 64 of the
+    512 work items); the other groups are covered row by row above."""
+    wl = inputs.config(5)
+    cache = gs.device_cache(wl, wl.cache_lens, fill_on_gpu=True)
+    _every_output(wl, cache=cache, groups=[(0, 0), (1, 3), (2, 5), (3, 7)])
 
 
 def test_long_streams_split_by_round_model_full_size():

@@ -144,7 +144,7 @@ def test_streaming_replay_equals_prefill_text():
 
 
 # ---------------------------------------------------------------------------
-# full-size thinker workloads (sampled rows)
+# full-size thinker workloads
 
 def test_thinker_prefill_full_size():
     """The thinker's pass at full size (128 interleaved units, GQA 40/8, each
@@ -163,6 +163,20 @@ def test_thinker_prefill_full_size():
     ref, ref_lse = gs.run_oracle(wl, rows=rows)
     gs.assert_close(gs.compare(out, lse, ref, ref_lse, rows=rows))
     assert torch.isfinite(out).all()
+
+
+def test_thinker_prefill_every_output():
+    """The thinker's pass at full size on every output element and lse,
+    against the block-wise fp64 oracle."""
+    wl = inputs.thinker_prefill()
+    cache = gs.device_cache(wl, [wl.Lq], fill_on_gpu=True)
+    gs.say(f"[gpu] {wl.name}: full size, every output")
+    out, lse = gs.run_gpu(wl, cache=cache)
+    torch.cuda.synchronize()
+    ref, ref_lse = gs.run_block_oracle(wl)
+    stats = gs.compare_all(out, lse, ref, ref_lse)
+    gs.say(f"[gpu]   {stats}")
+    gs.assert_close(stats)
 
 
 def test_thinker_decode_step_full_size():

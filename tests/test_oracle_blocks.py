@@ -1,15 +1,17 @@
-"""Pins of the block-wise fp64 gradient oracle (``oracle.bwd_blocks``), used
-to check the full-size backward element by element.  It must agree with the
-plain-loop oracle's gradients (itself pinned by autograd, central
-differences and planted mistakes) and with autograd of an explicitly masked
-softmax attention, on ragged, empty, unit, token-causal and grouped-query
-cases (training uses the same causal format, Sec. 2.3)."""
+"""Pins of the block-wise fp64 oracle (``oracle.blocks``), used to check
+full-size workloads on every output element and the full-size backward
+element by element.  Forward and gradients must agree with the plain-loop
+oracle (itself pinned by brute force, textbook cases, autograd, central
+differences and planted mistakes) within 1e-12, and the gradients with
+autograd of an explicitly masked softmax attention, on ragged, empty, unit,
+single-block, token-causal, grouped-query and padded cases (Abstract, Fig.
+1; Sec. 2.3 and Sec. 2.4)."""
 import numpy as np
 import pytest
 import torch
 
 import oracle
-from oracle import bwd_blocks
+from oracle import blocks
 
 
 def _case(seed, B, L, Hq, Hkv, d, nb, empty=False):
@@ -50,7 +52,7 @@ def test_blocks_match_loop_oracle(c, text):
     ts = _text_starts(np.random.default_rng([c["seed"], 6]), offs) if text else None
     scale = 0.11
     ref = oracle.prefill_bwd(q, k, v, do, offs, scale, text_starts=ts)
-    got = bwd_blocks.prefill_bwd(q, k, v, do, offs, scale, text_starts=ts)
+    got = blocks.prefill_bwd(q, k, v, do, offs, scale, text_starts=ts)
     for name, a, r in zip(("dq", "dk", "dv"), got, ref):
         err = np.abs(a - r).max()
         assert err <= 1e-12 * max(1.0, np.abs(r).max()), (name, err)
@@ -82,7 +84,7 @@ def test_blocks_match_autograd_of_a_dense_mask():
     S = S.masked_fill(~torch.from_numpy(mask), float("-inf"))
     O = torch.einsum("hij,jhc->ihc", torch.softmax(S, dim=-1), Vx)
     O.backward(torch.from_numpy(do[0]))
-    got = bwd_blocks.prefill_bwd(q, k, v, do, offs, scale, text_starts=ts)
+    got = blocks.prefill_bwd(q, k, v, do, offs, scale, text_starts=ts)
     for a, r in zip(got, (Q.grad, K.grad, V.grad)):
         assert np.abs(a[0] - r.numpy()).max() <= 1e-12
 
@@ -91,10 +93,10 @@ def test_partial_groups_are_exact_where_stated():
     q, k, v, do, offs = _case(seed=11, B=2, L=120, Hq=4, Hkv=2, d=64, nb=6, empty=True)
     ts = _text_starts(np.random.default_rng([11, 6]), offs)
     scale = 0.09
-    full = bwd_blocks.prefill_bwd(q, k, v, do, offs, scale, text_starts=ts)
+    full = blocks.prefill_bwd(q, k, v, do, offs, scale, text_starts=ts)
     for b, g, n0 in ((0, 1, 0), (1, 0, 4), (1, 1, 6)):
         lo = offs[b, n0]
-        dq, dk, dv = bwd_blocks.prefill_bwd_group(q, k, v, do, offs, scale, b, g, n0, text_starts=ts)
+        dq, dk, dv = blocks.prefill_bwd_group(q, k, v, do, offs, scale, b, g, n0, text_starts=ts)
         np.testing.assert_allclose(dq, full[0][b, lo:, 2 * g:2 * g + 2], rtol=0, atol=1e-13)
         np.testing.assert_allclose(dk, full[1][b, lo:, g], rtol=0, atol=1e-13)
         np.testing.assert_allclose(dv, full[2][b, lo:, g], rtol=0, atol=1e-13)
@@ -104,8 +106,41 @@ def test_dq_rows_match_the_full_gradient():
     q, k, v, do, offs = _case(seed=13, B=2, L=90, Hq=6, Hkv=3, d=64, nb=5, empty=True)
     ts = _text_starts(np.random.default_rng([13, 6]), offs)
     scale = 0.13
-    dq = bwd_blocks.prefill_bwd(q, k, v, do, offs, scale, text_starts=ts)[0]
+    dq = blocks.prefill_bwd(q, k, v, do, offs, scale, text_starts=ts)[0]
     g = np.random.default_rng(14)
     rows = np.stack([g.integers(0, 2, 40), g.integers(0, 6, 40), g.integers(0, 90, 40)], axis=1)
-    got = bwd_blocks.prefill_dq_rows(q, k, v, do, offs, scale, rows, text_starts=ts)
+    got = blocks.prefill_dq_rows(q, k, v, do, offs, scale, rows, text_starts=ts)
     np.testing.assert_allclose(got, dq[rows[:, 0], rows[:, 2], rows[:, 1]], rtol=0, atol=1e-13)
+
+
+@pytest.mark.parametrize("text", [False, True])
+@pytest.mark.parametrize("c", CASES, ids=lambda c: f"s{c['seed']}")
+def test_block_forward_matches_loop_oracle(c, text):
+    q, k, v, _, offs = _case(**c)
+    ts = _text_starts(np.random.default_rng([c["seed"], 6]), offs) if text else None
+    ro, rl = oracle.prefill(q, k, v, offs, 0.11, text_starts=ts)
+    go, gl = blocks.prefill(q, k, v, offs, 0.11, text_starts=ts)
+    assert np.abs(go - ro).max() <= 1e-12 * max(1.0, np.abs(ro).max())
+    assert np.abs(gl - rl).max() <= 1e-12 * max(1.0, np.abs(rl).max())
+
+
+@pytest.mark.parametrize("text,padded", [(False, False), (True, False), (False, True), (True, True)])
+def test_block_step_matches_loop_oracle(text, padded):
+    g = np.random.default_rng([21, int(text), int(padded)])
+    B, Lq, Hq, Hkv, d = 3, 37, 8, 2, 64
+    lens = np.array([0, 130, 301])
+    Lc = int(lens.max())
+    q = g.standard_normal((B, Lq, Hq, d))
+    kc = g.standard_normal((B, Lc, Hkv, d))
+    vc = g.standard_normal((B, Lc, Hkv, d))
+    kn = g.standard_normal((B, Lq, Hkv, d))
+    vn = g.standard_normal((B, Lq, Hkv, d))
+    ts = np.array([0, 17, Lq], np.int32) if text else None
+    nl = np.array([Lq, 20, 1], np.int32) if padded else None
+    ro, rl = oracle.step(q, kc, vc, lens, kn, vn, 0.125, text_starts=ts, new_lens=nl)
+    go, gl = blocks.step(q, kc, vc, lens, kn, vn, 0.125, text_starts=ts, new_lens=nl, row_chunk=50)
+    for b in range(B):
+        n = Lq if nl is None else int(nl[b])
+        assert np.abs(go[b, :n] - ro[b, :n]).max() <= 1e-12 * max(1.0, np.abs(ro[b, :n]).max())
+        assert np.abs(gl[b, :, :n] - rl[b, :, :n]).max() <= 1e-12 * max(1.0, np.abs(rl[b, :, :n]).max())
+        assert np.isnan(go[b, n:]).all()
