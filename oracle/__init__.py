@@ -14,6 +14,9 @@ Python binding never import it.
 * ``kv_append`` / ``gather`` are the paged full-history cache written out as
   plain per-token loops (the performer appends each received KV slice to its
   own full-history cache, Sec. 2.4).
+* ``oracle.blocks`` computes the same outputs, lse and gradients one query
+  block at a time with fp64 matmuls, for full-size checks of every element
+  (pinned to the loops above).
 
 Inputs are numpy arrays: float64, or uint16 holding bf16 bit patterns (which
 the C code widens exactly).  All token tensors are contiguous [B][L][H][d].
