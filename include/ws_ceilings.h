@@ -20,13 +20,14 @@ extern "C" {
 
 /*
  * wsc_mfma_loop -- dense bf16 matrix-core ceiling.  num_groups work-groups
- * of 8 waves (two per SIMD); each wave issues iters x 4 independent
+ * of 8 waves (two per SIMD); each wave issues iters x 4 x chains
  * v_mfma_f32_32x32x16_bf16 (32 x 32 x 16 multiply-adds each) on register
- * operands, no memory traffic in the loop.  Work: num_groups * 8 * iters *
- * 4 * 32768 flops.  out: device f32 [num_groups] (one checksum per
- * work-group, so the loop is not removed).  num_groups >= 1, iters >= 1.
+ * operands, into `chains` (1..4) independent accumulators, no memory
+ * traffic in the loop.  Work: num_groups * 8 * iters * 4 * chains * 32768
+ * flops.  out: device f32 [num_groups] (one checksum per work-group, so the
+ * loop is not removed).  num_groups >= 1, iters >= 1, 1 <= chains <= 4.
  */
-int wsc_mfma_loop(float *out, int32_t num_groups, int32_t iters, void *stream);
+int wsc_mfma_loop(float *out, int32_t num_groups, int32_t iters, int32_t chains, void *stream);
 
 /*
  * wsc_stream_read -- streaming HBM read ceiling.  Reads `bytes` bytes of

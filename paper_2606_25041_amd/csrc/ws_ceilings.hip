@@ -12,10 +12,11 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int CHAINS = 4;   // independent accumulators per wave
-
-// Two waves per SIMD, four dependency chains per wave: the matrix core of
-// every SIMD always has an MFMA ready to issue.
+// Two waves per SIMD, C independent dependency chains per wave: dependent
+// accumulation is cheap on this matrix core, and the rate of the loop
+// depends a little on the chain count, so the benchmark takes the best of
+// several.
+template <int C>
 __global__ __launch_bounds__(512) void mfma_loop_kernel(float *out, int iters) {
     const int lane = threadIdx.x & 63;
     bf16x8 a, b;
@@ -24,18 +25,20 @@ __global__ __launch_bounds__(512) void mfma_loop_kernel(float *out, int iters) {
         a[e] = (__bf16)(0.001f * (float)((lane * 8 + e) % 17));
         b[e] = (__bf16)(0.001f * (float)((lane * 5 + e) % 13));
     }
-    f32x16 acc[CHAINS];
+    f32x16 acc[C];
 #pragma unroll
-    for (int c = 0; c < CHAINS; ++c)
+    for (int c = 0; c < C; ++c)
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[c][v] = 0.f;
     for (int i = 0; i < iters; ++i) {
 #pragma unroll
-        for (int c = 0; c < CHAINS; ++c) acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[c], 0, 0, 0);
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+            for (int c = 0; c < C; ++c) acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[c], 0, 0, 0);
     }
     float s = 0.f;
 #pragma unroll
-    for (int c = 0; c < CHAINS; ++c)
+    for (int c = 0; c < C; ++c)
 #pragma unroll
         for (int v = 0; v < 16; ++v) s += acc[c][v];
     __shared__ float red[512];
@@ -76,10 +79,12 @@ __global__ __launch_bounds__(256) void stream_read_kernel(const u32x4 *src, uint
 
 extern "C" {
 
-int wsc_mfma_loop(float *out, int32_t num_groups, int32_t iters, void *stream) {
-    if (!out || num_groups < 1 || iters < 1) return (int)hipErrorInvalidValue;
-    hipLaunchKernelGGL(mfma_loop_kernel, dim3((unsigned)num_groups), dim3(512), 0, (hipStream_t)stream, out,
-                       (int)iters);
+int wsc_mfma_loop(float *out, int32_t num_groups, int32_t iters, int32_t chains, void *stream) {
+    if (!out || num_groups < 1 || iters < 1 || chains < 1 || chains > 4) return (int)hipErrorInvalidValue;
+    void (*k)(float *, int) = chains == 1 ? mfma_loop_kernel<1>
+                            : chains == 2 ? mfma_loop_kernel<2>
+                            : chains == 3 ? mfma_loop_kernel<3> : mfma_loop_kernel<4>;
+    hipLaunchKernelGGL(k, dim3((unsigned)num_groups), dim3(512), 0, (hipStream_t)stream, out, (int)iters);
     return (int)hipGetLastError();
 }
 

@@ -67,9 +67,11 @@ def test_ceilings_library_exports_every_declared_symbol():
     # argument checks fail before anything is launched
     lib.wsc_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int32,
                                     ctypes.c_void_p]
-    lib.wsc_mfma_loop.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p]
+    lib.wsc_mfma_loop.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p]
     assert lib.wsc_stream_read(FAKE, 17, FAKE, 1, None) != 0
-    assert lib.wsc_mfma_loop(None, 1, 1, None) != 0
+    assert lib.wsc_mfma_loop(None, 1, 1, 2, None) != 0
+    assert lib.wsc_mfma_loop(FAKE, 1, 1, 0, None) != 0
+    assert lib.wsc_mfma_loop(FAKE, 1, 1, 5, None) != 0
 
 
 def t4(ptr=FAKE, dtype=ws.WS_DTYPE_BF16, sb=0, st=0, sh=0, d=128, L=16, H=4):
