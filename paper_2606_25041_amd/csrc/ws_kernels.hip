@@ -48,6 +48,7 @@ namespace {
 
 constexpr int KT = 64;        // keys per tile (= page size)
 constexpr float RESCALE_LOG2 = 8.f;  // lazy-rescale threshold (log2 units)
+constexpr float RESCALE_BOUND = 256.f;  // 2^RESCALE_LOG2
 constexpr int PAGE_LDS = 2560;       // page ids of a split staged in LDS (more: read from memory)
 constexpr int NSTAGE = 4;            // K/V tiles resident in the LDS ring
 
@@ -413,10 +414,10 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     // 8 * (ks4 & 1) + e % 8 of key block ks4 / 2)
     auto score = [&](const Tile &sc, int e) -> float { return sc[e >> 5][(e >> 4) & 1][e & 15]; };
     // P weights of a tile: 2^(s * c2 - m), rounded to bf16 for P.V, and their
-    // fp32 row sums (so lse is exact to fp32 rounding).  One straight block:
+    // fp32 lane sums ls (so lse is exact to fp32 rounding).  One straight block:
     // all exponents, then all exps, then the packs and a pairwise sum, so
     // the dependent steps of different scores overlap.
-    auto softmax_weights = [&](const Tile &sc, bf16x8 (&pf)[NB][4], const float (&m_use)[NB]) {
+    auto softmax_weights = [&](const Tile &sc, bf16x8 (&pf)[NB][4], const float (&m_use)[NB], float (&ls)[NB]) {
 #pragma unroll
         for (int n = 0; n < NB; ++n) {
             float x[32];
@@ -431,7 +432,7 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
             for (int w = 1; w < 32; w *= 2)
 #pragma unroll
                 for (int f = 0; f < 32; f += 2 * w) x[f] += x[f + w];
-            l[n] += x[0];
+            ls[n] = x[0];
         }
     };
     // in-lane max of a tile's scores per query block; the other half-wave's
@@ -516,12 +517,27 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
             asm volatile("" ::: "memory");
             mask(t, sc);
         }
-        float mx[NB];
-        lane_max(sc, mx);
-        update_max(mx);
-        float m_use[NB];
+        // Weights at the running max as it stands; the tile's max is only
+        // taken when some row may need a larger one: a row that has seen no
+        // key yet, or whose lane sum of weights exceeds 2^RESCALE_LOG2 (a
+        // necessary condition for a score above m + RESCALE_LOG2; inf and
+        // NaN land here too).  That path is the lazy-rescale update and the
+        // weights again, so every weight stays <= 2^RESCALE_LOG2 either way.
+        float m_use[NB], ls[NB];
         max_shift(m_use);
-        softmax_weights(sc, pf, m_use);
+        softmax_weights(sc, pf, m_use, ls);
+        bool slow = false;
+#pragma unroll
+        for (int n = 0; n < NB; ++n) slow = slow || m[n] == -INFINITY || !(ls[n] <= RESCALE_BOUND);
+        if (__builtin_amdgcn_ballot_w64(slow)) {
+            float mx[NB];
+            lane_max(sc, mx);
+            update_max(mx);
+            max_shift(m_use);
+            softmax_weights(sc, pf, m_use, ls);
+        }
+#pragma unroll
+        for (int n = 0; n < NB; ++n) l[n] += ls[n];
     };
     // O^T[d][query] += V^T P^T from the V tile of a stage; V reads two steps
     // ahead of their MFMAs
@@ -542,8 +558,8 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
 
     // ---- pipeline ---------------------------------------------------------
     // Tile t lives in ring stage (t - t_begin) % NSTAGE.  Every wave runs
-    // the same loop: step j is an MFMA block (O += P V of tile j-1, then S^T
-    // of tile j), a work-group barrier, the VALU block (softmax of tile j)
+    // the same loop: step j is an MFMA block (S^T of tile j, then O += P V
+    // of tile j-1), a work-group barrier, the VALU block (softmax of tile j)
     // and another barrier.  The second wave on each SIMD (waves NWD..NW-1,
     // SIMD = wave % 4) enters the loop one barrier late, so on every SIMD one
     // wave's softmax overlaps the other wave's MFMAs.  The leading waves
@@ -603,8 +619,10 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
             // pipeline needs.
             asm volatile("" : "+v"(kbase), "+v"(vbase[0]), "+v"(vbase[1]), "+v"(lofs_p), "+v"(lofs_k), "+v"(lofs_v));
             if (busy) {
-                if (j > t_begin) pv(stage_off(j - 1), pf);
+                // S^T of tile j first: its accumulators are complete long
+                // before the softmax reads them after the barrier
                 if (j < t_end) qk(stage_off(j), S);
+                if (j > t_begin) pv(stage_off(j - 1), pf);
             }
             wg_barrier();
             // the leading waves issue the loads of tile j+2 here, ahead of
