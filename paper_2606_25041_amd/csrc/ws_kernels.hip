@@ -51,6 +51,7 @@ constexpr float RESCALE_LOG2 = 8.f;  // lazy-rescale threshold (log2 units)
 constexpr float RESCALE_BOUND = 256.f;  // 2^RESCALE_LOG2
 constexpr int PAGE_LDS = 2560;       // page ids of a split staged in LDS (more: read from memory)
 constexpr int NSTAGE = 4;            // K/V tiles resident in the LDS ring
+constexpr int RAHEAD = 4;            // LDS operand reads issued this many MFMAs ahead
 
 // The fused append's share of step work item ai (of nqt * nsplit per
 // (stream, KV head)): the group's items split the new tokens evenly; tokens
@@ -487,8 +488,8 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
         for (int n = 0; n < NB; ++n) m_use[n] = (m[n] == -INFINITY) ? 0.f : m[n];
     };
     // S^T[key][query] = K Q^T for the 64 keys of a stage x this wave's
-    // 32 * NB queries.  Each step is fenced so the reads stay two steps ahead
-    // of their MFMAs.
+    // 32 * NB queries.  Each step is fenced so the reads stay RAHEAD steps
+    // ahead of their MFMAs.
     auto qk = [&](uint32_t soff, Tile &sn) {
         const uint32_t kb = kbase + soff;
 #pragma unroll
@@ -497,15 +498,15 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
             for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) sn[n][mb][v] = 0.f;
-        bf16x8 kf[3];
-        kf[0] = kread(kb, 0);
-        kf[1] = kread(kb, 1);
+        bf16x8 kf[RAHEAD + 1];
+#pragma unroll
+        for (int i = 0; i < RAHEAD; ++i) kf[i] = kread(kb, i);
 #pragma unroll
         for (int i = 0; i < NQK; ++i) {
-            if (i + 2 < NQK) kf[(i + 2) % 3] = kread(kb, i + 2);
+            if (i + RAHEAD < NQK) kf[(i + RAHEAD) % (RAHEAD + 1)] = kread(kb, i + RAHEAD);
 #pragma unroll
             for (int n = 0; n < NB; ++n)
-                sn[n][i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[n][i >> 1], sn[n][i & 1], 0, 0, 0);
+                sn[n][i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % (RAHEAD + 1)], qf[n][i >> 1], sn[n][i & 1], 0, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
         }
     };
@@ -539,19 +540,19 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
 #pragma unroll
         for (int n = 0; n < NB; ++n) l[n] += ls[n];
     };
-    // O^T[d][query] += V^T P^T from the V tile of a stage; V reads two steps
-    // ahead of their MFMAs
+    // O^T[d][query] += V^T P^T from the V tile of a stage; V reads RAHEAD
+    // steps ahead of their MFMAs
     auto pv = [&](uint32_t soff, const bf16x8 (&pf)[NB][4]) {
         const uint32_t v0 = vbase[0] + soff, v1 = vbase[1] + soff;
-        bf16x8 vf[3];
-        vf[0] = vread(v0, v1, 0);
-        vf[1] = vread(v0, v1, 1);
+        bf16x8 vf[RAHEAD + 1];
+#pragma unroll
+        for (int i = 0; i < RAHEAD; ++i) vf[i] = vread(v0, v1, i);
 #pragma unroll
         for (int i = 0; i < NPV; ++i) {
-            if (i + 2 < NPV) vf[(i + 2) % 3] = vread(v0, v1, i + 2);
+            if (i + RAHEAD < NPV) vf[(i + RAHEAD) % (RAHEAD + 1)] = vread(v0, v1, i + RAHEAD);
 #pragma unroll
             for (int n = 0; n < NB; ++n)
-                o[n][i % MD] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i % 3], pf[n][i / MD], o[n][i % MD], 0, 0, 0);
+                o[n][i % MD] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i % (RAHEAD + 1)], pf[n][i / MD], o[n][i % MD], 0, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
         }
     };
