@@ -72,12 +72,12 @@ def _check_every_output(wl, cache=None):
     return stats
 
 
-@pytest.mark.parametrize("profile", ["rising", "mixed"])
-def test_prefill_running_max_paths(profile):
+@pytest.mark.parametrize("profile,D", [("rising", 128), ("mixed", 128), ("mixed", 64)])
+def test_prefill_running_max_paths(profile, D):
     # stream 1's first block lies inside the first tile: its rows see no
     # key above the first tile's level
     lens = [np.array([100, 300, 77, 400, 223]), np.array([40, 600, 60, 300, 100])]
-    wl = inputs.prefill_workload(f"softmax_paths_prefill_{profile}", 2, 4, 2, 128, lens, 5101)
+    wl = inputs.prefill_workload(f"softmax_paths_prefill_{profile}_d{D}", 2, 4, 2, D, lens, 5101)
     _shape(wl, profile, lambda b: np.arange(wl.Lq))
     _check_every_output(wl)
 
