@@ -49,8 +49,7 @@ namespace {
 constexpr int KT = 64;        // keys per tile (= page size)
 constexpr float RESCALE_LOG2 = 8.f;  // lazy-rescale threshold (log2 units)
 constexpr float RESCALE_BOUND = 256.f;  // 2^RESCALE_LOG2
-constexpr int PAGE_LDS = 2560;       // page ids of a split staged in LDS (more: read from memory)
-constexpr int NSTAGE = 4;            // K/V tiles resident in the LDS ring
+constexpr int NSTAGE = 5;            // K/V tiles resident in the LDS ring (loads three tiles ahead)
 constexpr int RAHEAD = 4;            // LDS operand reads issued this many MFMAs ahead
 
 // The fused append's share of step work item ai (of nqt * nsplit per
@@ -87,7 +86,6 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     constexpr int VRING = NSTAGE * TILEB;  // byte offset of the V ring
     static_assert(NI >= 1 && TILEB % (NWD * 1024) == 0, "a tile splits into wave-wide loads");
     __shared__ __attribute__((aligned(1024))) char smem[2 * NSTAGE * TILEB];
-    __shared__ int page_lds[PAGE_LDS];
 
     // ---- work item ------------------------------------------------------
     // The launch parameters the decode and the query loads need are read in
@@ -163,14 +161,14 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
 
     // Query rows of this wave go global -> LDS -> registers, issued first
     // thing: the direct loads stay in order with the tile loads, so one
-    // counted wait covers both.  They are staged in ring stages 2 and 3 (of
-    // the K ring for waves 0..3, of the V ring for waves 4..7), which are
-    // first refilled in loop step t_begin, after every wave has passed the
-    // prologue barrier.  The layout is that of a key tile, so the fragments
+    // counted wait covers both.  They are staged in the last two ring stages
+    // (of the K ring for waves 0..3, of the V ring for waves 4..7), which are
+    // first refilled in loop steps t_begin and t_begin + 1, after every wave
+    // has passed the prologue barrier.  The layout is that of a key tile, so the fragments
     // are read like K.
     static_assert(NB == 1, "query staging holds 32 rows per wave");
     constexpr int QI = 32 * ROWB / 1024;   // wave-wide loads per wave
-    const uint32_t q_stage = (uint32_t)((wave < 4 ? 0 : VRING) + 2 * TILEB + (wave & 3) * 32 * ROWB);
+    const uint32_t q_stage = (uint32_t)((wave < 4 ? 0 : VRING) + (NSTAGE - 2) * TILEB + (wave & 3) * 32 * ROWB);
     {
         const char *qg = (const char *)(qptr + b * q_sb);
 #pragma unroll
@@ -213,17 +211,12 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     const int t_end = (int)fastdiv((split + 1) * (uint32_t)ntile, fd_split);
 
     // ---- page ids -------------------------------------------------------
-    // The first three tiles' pages are read up front; the rest of the
-    // split's page ids are staged in LDS once, so no page-table read sits in
-    // front of a later tile's loads.
+    // The first four tiles' pages are read up front; later ones one loop
+    // step before their tile's loads are issued (a scalar load, waited for
+    // with the tile loads), so no page-table read sits in front of them.
     const int32_t *ptab = a.page_table + (int64_t)b * a.max_pages;
     const int tp_end = min(t_end, (n_pool + KT - 1) / KT);   // tiles with cache rows
     auto page_glb = [&](int t) -> int { return t < tp_end ? ld_uniform(ptab, t) : 0; };
-    const int n_lds_pages = min(max(tp_end - t_begin, 0), PAGE_LDS);
-    auto page_of = [&](int t) -> int {
-        const int i = t - t_begin;
-        return i < PAGE_LDS ? __builtin_amdgcn_readfirstlane(page_lds[i]) : page_glb(t);
-    };
 
     // ---- this lane's query rows -------------------------------------------
     // row n of the lane: q0 + rblk * 32 * NB + 32 * n + l32 (the fragments
@@ -564,10 +557,10 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     // and another barrier.  The second wave on each SIMD (waves NWD..NW-1,
     // SIMD = wave % 4) enters the loop one barrier late, so on every SIMD one
     // wave's softmax overlaps the other wave's MFMAs.  The leading waves
-    // issue the loads of tile j+2 at the start of step j and wait for tile
+    // issue the loads of tile j+3 at the start of step j and wait for tile
     // j+1 before its last barrier: a stage is refilled only after the
-    // trailing waves' last read of its tile, and its loads have two steps to
-    // land.
+    // trailing waves' last read of its tile, and its loads have three steps
+    // to land.
     static_assert(NW == 8, "two waves per SIMD");
     const bool lead = wave < NWD;
     // a wave whose 32 rows all lie past the last row (a small block's tile)
@@ -578,36 +571,22 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
     const int n_tiles = t_end - t_begin;
     auto stage_off = [&](int t) -> uint32_t { return (uint32_t)((t - t_begin) % NSTAGE) * TILEB; };
     if (n_tiles > 0) {
-        // Prologue: the leading waves issue the first two tiles and wait for
-        // the first and their query rows (the second tile stays in flight
-        // into loop step t_begin, as in the steady state); the trailing waves
-        // stage the split's page ids in LDS.  The page-id reads are the only
+        // Prologue: the leading waves issue the first three tiles and wait
+        // for the first and their query rows (the other two stay in flight
+        // into loop step t_begin, as in the steady state); the trailing
+        // waves wait for their query rows.  The page-id reads are the only
         // loads the compiler sees here, so its own waits never cover the
         // tile loads.
-        int pg_next = 0;   // page of tile j+2, read one step ahead
+        int pg_next = 0;   // page of tile j+3, read one step ahead
         if (lead) {
-            const int pg0 = page_glb(t_begin), pg1 = page_glb(t_begin + 1);
-            pg_next = page_glb(t_begin + 2);
+            const int pg0 = page_glb(t_begin), pg1 = page_glb(t_begin + 1), pg2 = page_glb(t_begin + 2);
+            pg_next = page_glb(t_begin + 3);
             issue_tile(t_begin, 0, pg0);
-            if (n_tiles > 1) {
-                issue_tile(t_begin + 1, 1, pg1);
-                wait_vm_lgkm<2 * NI>();
-            } else {
-                wait_vm_lgkm<0>();
-            }
+            if (n_tiles > 1) issue_tile(t_begin + 1, 1, pg1);
+            if (n_tiles > 2) issue_tile(t_begin + 2, 2, pg2);
+            wait_tiles(min(2, n_tiles - 1));
         } else {
-            constexpr int NPT = PAGE_LDS / (NT / 2);
-            const int ti = tid - NT / 2;
-            int pre[NPT];
-#pragma unroll
-            for (int k = 0; k < NPT; ++k) {
-                const int i = ti + k * (NT / 2);
-                pre[k] = i < n_lds_pages ? ptab[t_begin + i] : 0;
-            }
             wait_vm_lgkm<0>();
-#pragma unroll
-            for (int k = 0; k < NPT; ++k)
-                if (ti + k * (NT / 2) < n_lds_pages) page_lds[ti + k * (NT / 2)] = pre[k];
         }
         read_q();
         wait_vm_lgkm<63>();   // (LDS reads and writes complete; no vector-memory wait)
@@ -626,14 +605,15 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(const AttnArgs a) {
                 if (j > t_begin) pv(stage_off(j - 1), pf);
             }
             wg_barrier();
-            // the leading waves issue the loads of tile j+2 here, ahead of
+            // the leading waves issue the loads of tile j+3 here, ahead of
             // their softmax, rather than ahead of their MFMA block
-            if (lead && j + 2 < t_end) issue_tile(j + 2, (j + 2 - t_begin) % NSTAGE, pg_next);
+            if (lead && j + 3 < t_end) issue_tile(j + 3, (j + 3 - t_begin) % NSTAGE, pg_next);
             if (busy && j < t_end) softmax(j, S, pf);
-            // (read here, under the wait below: a scalar or LDS read left in
-            // flight across the MFMA block would force full LDS drains there)
-            if (lead && j + 3 < t_end) pg_next = page_of(j + 3);
-            if (lead && j + 1 < t_end) wait_tiles(j + 2 < t_end ? 1 : 0);
+            // (read here, under the wait below: a scalar read left in flight
+            // across the MFMA block would force full LDS drains there)
+            if (lead && j + 4 < t_end) pg_next = page_glb(j + 4);
+            // tile j+1 landed; tiles j+2 and j+3 may stay in flight
+            if (lead && j + 1 < t_end) wait_tiles(min(2, t_end - 2 - j));
             wg_barrier();
         }
         if (lead) wg_barrier();

@@ -228,19 +228,17 @@ def test_long_streams_split_by_round_model_full_size():
 
 
 def test_long_split_reads_page_ids_from_memory():
-    """One KV split longer than the page ids the kernel stages in LDS (2560
-    tiles = 163840 tokens): 170000 cached tokens in shuffled pages, one KV
-    head shared by 8 query heads, 8192 new tokens (65536 packed rows = 256
-    query tiles, exactly one round of work-groups on 256 compute units, so
-    the plan keeps one split); the pages past the staged ids are looked up
-    in the device page table.  One row of every packed 32-row block (each
-    sees every key)."""
+    """One long KV split: 170000 cached tokens (2657 pages) in shuffled
+    pages, one KV head shared by 8 query heads, 8192 new tokens (65536
+    packed rows = 256 query tiles, exactly one round of work-groups on 256
+    compute units, so the plan keeps one split); every page id is read from
+    the device page table one loop step before its tile's loads.  One row of
+    every packed 32-row block (each sees every key)."""
     wl = inputs.step_workload("step_long_split_b1_gqa8x1_q8192_c170000", 1, 8, 1, 128, 8192, [170000],
                               seed=77, fuse_append=True)
     ns, _ = ws.step_plan(1, 8, 1, 8192, wl.cache_lens)
     if ns != 1:
         pytest.skip(f"the device plan splits this step in {ns}")
-    assert (170000 + 63) // 64 > 2560
     cache = gs.device_cache(wl, wl.cache_lens, fill_on_gpu=True)
     rows = gs.coverage_rows_step(np.random.default_rng(8), wl.B, wl.Hq, wl.Hkv, wl.Lq, must=[(0, 7, 8191)])
     _covered(wl, cache, rows)
