@@ -17,18 +17,19 @@
 //    owns one query column and 16 keys, so row max/sum are in-lane plus one
 //    v_permlane32_swap per 64-key tile.
 //  * Online softmax in the log2 domain (scale*log2(e) folded into one FMA),
-//    fp32 running max/sum per lane, lazy rescale of O.
+//    fp32 running max/sum per lane, lazy rescale of O; a tile's max is only
+//    taken when some row may need a larger running max.
 //  * O^T += V^T P^T on the same MFMA: P stays in registers (the accumulator
 //    layout of S^T is exactly the B-operand layout once the 16 keys of each
 //    MFMA step are permuted consistently on both operands); V is read with
 //    ds_read_b64_tr_b16 from a row-major LDS tile, so no transpose pass.
 //  * K/V tiles of 64 keys (= one cache page) go from global memory straight
-//    into a 4-stage LDS ring (global_load_lds_dwordx4), two tiles in flight
+//    into a 5-stage LDS ring (global_load_lds_dwordx4), three tiles in flight
 //    while the current one is used; rows are XOR-swizzled in 16-byte chunks
 //    so both the K reads and the V transpose reads are bank-conflict free.
 //  * Two waves share each SIMD and run the same loop one block apart: while
-//    one issues the MFMAs of a tile (P V of the previous tile, S^T of this
-//    one), the other computes its softmax; a work-group barrier separates
+//    one issues the MFMAs of a tile (S^T of this one, P V of the previous
+//    tile), the other computes its softmax; a work-group barrier separates
 //    the blocks.
 //  * Tiles past the last visible key of the query tile are never loaded
 //    (block-granularity skip); tiles fully visible to every row of the query
