@@ -124,9 +124,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * TILEB];   // [stage][K, V]
     const int nqt = (a.L + 127) / 128;
     const int wid = blockIdx.x;
-    const int qt = nqt - 1 - wid % nqt;   // heavy tiles first
-    const int h = (wid / nqt) % a.Hq;
-    const int b = wid / (nqt * a.Hq);
+    // query tiles heaviest first over all (stream, head) pairs, so the
+    // dispatch order is longest-first across the whole launch and the last
+    // round of work-groups holds the shortest tiles
+    const int qt = nqt - 1 - wid / (a.B * a.Hq);
+    const int h = (wid % (a.B * a.Hq)) % a.Hq;
+    const int b = (wid % (a.B * a.Hq)) / a.Hq;
     const int g = h / a.G;
     const int tid = threadIdx.x, lane = tid & 63, hf = lane >> 5, l32 = lane & 31;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -246,9 +249,14 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(const BwdArgs a) {
     __shared__ __attribute__((aligned(16))) int skend[2][2][32];
     const int nkt = (a.L + 127) / 128;
     const int wid = blockIdx.x;
-    const int kt = wid % nkt;
-    const int kvh = (wid / nkt) % a.Hkv;
-    const int b = wid / (nkt * a.Hkv);
+    // key tiles from the first keys (seen by the most rows: the heaviest)
+    // over all (stream, KV head) groups, so the dispatch order is
+    // longest-first across the whole launch; consecutive work-groups are
+    // different groups, and work-group i runs on XCD i mod 8, so each XCD
+    // keeps the same groups (with 16 of them, two) for the whole launch
+    const int kt = wid / (a.B * a.Hkv);
+    const int kvh = (wid % (a.B * a.Hkv)) % a.Hkv;
+    const int b = (wid % (a.B * a.Hkv)) / a.Hkv;
     const int tid = threadIdx.x, lane = tid & 63, hf = lane >> 5, l32 = lane & 31;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int grp = wave >> 2, sub = wave & 3, gtid = tid & 255;
