@@ -126,10 +126,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const int wid = blockIdx.x;
     // query tiles heaviest first over all (stream, head) pairs, so the
     // dispatch order is longest-first across the whole launch and the last
-    // round of work-groups holds the shortest tiles
+    // round of work-groups holds the shortest tiles; within a tile level the
+    // (stream, KV head) group is the fast digit, so with work-group i on XCD
+    // i mod 8 the G query heads of a group share an XCD (and its L2) for
+    // the whole launch
     const int qt = nqt - 1 - wid / (a.B * a.Hq);
-    const int h = (wid % (a.B * a.Hq)) % a.Hq;
-    const int b = (wid % (a.B * a.Hq)) / a.Hq;
+    const int kq = wid % (a.B * a.Hq);
+    const int grp = kq % (a.B * a.Hkv), hhq = kq / (a.B * a.Hkv);
+    const int b = grp / a.Hkv;
+    const int h = (grp % a.Hkv) * a.G + hhq;
     const int g = h / a.G;
     const int tid = threadIdx.x, lane = tid & 63, hf = lane >> 5, l32 = lane & 31;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
