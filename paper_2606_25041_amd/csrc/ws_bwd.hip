@@ -11,6 +11,8 @@
 namespace ws {
 namespace {
 
+constexpr int KB_DKDV = 16;   // key tiles of one group taken together on an XCD (dK/dV)
+
 // ---------------------------------------------------------------------------
 // Gradients of the whole-sequence path (training shares the causal format,
 // Sec. 2.3).  With the forward's lse, P_ij = exp(s_ij - lse_i) needs no
@@ -254,14 +256,30 @@ __global__ __launch_bounds__(512) void bwd_dkdv_kernel(const BwdArgs a) {
     __shared__ __attribute__((aligned(16))) int skend[2][2][32];
     const int nkt = (a.L + 127) / 128;
     const int wid = blockIdx.x;
-    // key tiles from the first keys (seen by the most rows: the heaviest)
+    // Key tiles from the first keys (seen by the most rows: the heaviest)
     // over all (stream, KV head) groups, so the dispatch order is
-    // longest-first across the whole launch; consecutive work-groups are
-    // different groups, and work-group i runs on XCD i mod 8, so each XCD
-    // keeps the same groups (with 16 of them, two) for the whole launch
-    const int kt = wid / (a.B * a.Hkv);
-    const int kvh = (wid % (a.B * a.Hkv)) % a.Hkv;
-    const int b = (wid % (a.B * a.Hkv)) / a.Hkv;
+    // longest-first across the whole launch.  Work-group i runs on XCD
+    // i mod 8: when the group count is a multiple of 8, XCD x keeps groups
+    // x, x + 8, ... for the whole launch and takes their key tiles in blocks
+    // of KB_DKDV, the tiles of a block of one group one after another, so
+    // they start together and walk the same rows at about the same time
+    // (one L2 read serves them); the launch is rounded up to whole blocks
+    // and work-groups past the last key tile exit at once.
+    const int ngrp = a.B * a.Hkv;
+    int kt, grpi;
+    if (ngrp % NUM_XCD == 0) {
+        const int gpx = ngrp / NUM_XCD, x = wid % NUM_XCD, l = wid / NUM_XCD;
+        const int kb = l / (gpx * KB_DKDV), r = l - kb * gpx * KB_DKDV;
+        const int gi = r / KB_DKDV;
+        kt = kb * KB_DKDV + (r - gi * KB_DKDV);
+        grpi = x + NUM_XCD * gi;
+        if (kt >= nkt) return;
+    } else {
+        kt = wid / ngrp;
+        grpi = wid % ngrp;
+    }
+    const int kvh = grpi % a.Hkv;
+    const int b = grpi / a.Hkv;
     const int tid = threadIdx.x, lane = tid & 63, hf = lane >> 5, l32 = lane & 31;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int grp = wave >> 2, sub = wave & 3, gtid = tid & 255;
@@ -445,7 +463,9 @@ int launch_bwd_t(const BwdArgs &a, hipStream_t st) {
     const int64_t nqt = (a.L + 127) / 128;
     hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3((unsigned)(a.B * a.Hq * nqt)), dim3(256), 0, st, a);
     if (int e = (int)hipGetLastError()) return e;
-    hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3((unsigned)(a.B * a.Hkv * nqt)), dim3(512), 0, st, a);
+    const int64_t ngrp = (int64_t)a.B * a.Hkv;
+    const int64_t grid = ngrp % NUM_XCD == 0 ? ngrp * ((nqt + KB_DKDV - 1) / KB_DKDV) * KB_DKDV : ngrp * nqt;
+    hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3((unsigned)grid), dim3(512), 0, st, a);
     return (int)hipGetLastError();
 }
 
