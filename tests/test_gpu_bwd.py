@@ -55,6 +55,19 @@ def test_bwd_ragged_blocks(D, L, nb):
     _check(*_grad_case(f"bwd_d{D}_L{L}", 2, 4, 2, D, lens, seed=81 + L + D))
 
 
+def test_bwd_eight_kv_groups_partial_key_blocks():
+    """2 streams x 4 KV heads = 8 (stream, KV head) groups: the dK/dV kernel
+    takes each XCD's key tiles in blocks of 16 per group, and with 1000
+    tokens (8 key tiles of 128) half of every block lies past the last key
+    tile (those work-groups exit at once)."""
+    g = np.random.default_rng([1000, 98])
+    lens = []
+    for _ in range(2):
+        cuts = np.sort(g.choice(np.arange(1, 1000), size=6, replace=False))
+        lens.append(np.diff(np.concatenate([[0], cuts, [1000]])))
+    _check(*_grad_case("bwd_8groups_L1000", 2, 8, 4, 128, lens, seed=87))
+
+
 def test_bwd_unit_empty_and_long_blocks():
     lens = [np.array([1, 1, 0, 5, 1, 200, 0, 1, 90, 60])]
     _check(*_grad_case("bwd_unit_empty", 1, 2, 1, 128, lens, seed=83))
