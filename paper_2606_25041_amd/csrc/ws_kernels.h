@@ -77,11 +77,12 @@ struct AttnArgs {
     // row p = t * G + hh for token t and head kvh * G + hh, so small blocks
     // still fill the query tiles; nrows = G * Lq rows per (b, KV head).
     // split-KV partials (step only), in blocks of 32 packed rows (nrb =
-    // ceil(G * Lq / 32) blocks per (b, KV head)).  f32 output: o [S][B][Hq][nrb][D/4][64 lanes][4]
-    // f32 unnormalised, in the accumulator's register order, and (m, l)
-    // [S][B][Hq][nrb * 32][2].  bf16 output: o / l as bf16
-    // [S][B][Hq][nrb][D/8][64 lanes][8] in register order (two accumulator
-    // groups per lane) and m + log2(l) [S][B][Hq][nrb * 32] f32 at part_ml.
+    // ceil(G * Lq / 32) blocks per (b, KV head)).  f32 output: o
+    // [S][B][Hkv][nrb][D/4][64 lanes][4] f32 unnormalised, in the
+    // accumulator's register order, and (m, l) [S][B][Hkv][nrb * 32][2].
+    // bf16 output: o / l as bf16 [S][B][Hkv][nrb][D/8][64 lanes][8] in
+    // register order (two accumulator groups per lane) and m + log2(l)
+    // [S][B][Hkv][nrb * 32] f32 at part_ml.
     float *part_o, *part_ml;
     int32_t nrb;
     int32_t nrows;       // rows per item's head space: Lq (prefill) or G * Lq (step)
@@ -90,12 +91,12 @@ struct AttnArgs {
     int32_t mode;        // MODE_PREFILL or MODE_STEP
     int32_t paged;       // prefill only: keys/values come from the pool
     int32_t fuse_append; // step only: also commit kc/vc to the pool
-    int32_t nsplit;      // KV splits per (b, hq, q-tile)
-    int32_t nqt;         // q-tiles per (b, hq)
-    int32_t n_work;      // B * Hq * nqt * nsplit
+    int32_t nsplit;      // KV splits per query tile (1 in the prefill)
+    int32_t nqt;         // query tiles per head space: of Lq rows (prefill) or G * Lq packed rows (step)
+    int32_t n_work;      // B * Hkv * gi * nqt * nsplit
     int32_t per_xcd;     // ceil(n_work / 8)
-    int32_t per_group;   // G * nqt * nsplit: work items per (b, KV head)
-    int32_t per_qt;      // G * nsplit: work items per (b, KV head, q-tile)
+    int32_t per_group;   // gi * nqt * nsplit: work items per (b, KV head)
+    int32_t per_qt;      // gi * nsplit: work items per (b, KV head, q-tile)
     // dividers by per_group, per_qt, G, Hkv and nsplit
     FastDiv fd_group, fd_qt, fd_g, fd_hkv, fd_split;
     FastDiv fd_gq;       // divider by G (packed row -> token)

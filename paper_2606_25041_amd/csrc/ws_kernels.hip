@@ -10,8 +10,11 @@
 // gradient kernels, which serve training in the same causal format
 // (Sec. 2.3), are in ws_bwd.hip.
 //
-// Attention kernel design (one work-group = one (stream, query head,
-// query tile, KV split) work item; 8 waves x 32 query rows = 256 rows):
+// Attention kernel design (one work-group = one work item: a tile of 256
+// query rows of one (stream, KV head) group and one KV split, 8 waves x 32
+// rows; in the prefill the rows are tokens of one query head of the group,
+// in a step they are packed (token, query head) rows, every query head of
+// the group for consecutive new tokens):
 //  * S^T = K Q^T on v_mfma_f32_32x32x16_bf16: K (A operand) from LDS, Q (B
 //    operand) resident in registers.  In the 32x32 accumulator layout a lane
 //    owns one query column and 16 keys, so row max/sum are in-lane plus one
