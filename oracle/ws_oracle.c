@@ -605,7 +605,11 @@ static void *wso_bwd_worker(void *arg)
                         continue;
                     for (int c = 0; c < d; ++c)
                         dp[j] += wso_load(&dov, b, i, h, c) * wso_load(&J->v, b, j, g, c);
+#if WSO_MUTANT == 16
+                    D += dp[j];
+#else
                     D += p[j] * dp[j];
+#endif
                 }
                 /* dS_ij = P_ij (dP_ij - D_i) and the three gradients */
                 double *dqi = T->dq + (((int64_t)b * L + i) * J->Hq + h) * d;
@@ -622,13 +626,21 @@ static void *wso_bwd_worker(void *arg)
                     double *dkj = T->dk + (((int64_t)b * L + j) * J->Hkv + g) * d;
                     double *dvj = T->dv + (((int64_t)b * L + j) * J->Hkv + g) * d;
                     for (int c = 0; c < d; ++c) {
+#if WSO_MUTANT == 14
+                        dqi[c] += J->scale * ds * wso_load(&J->v, b, j, g, c);
+#else
                         dqi[c] += J->scale * ds * wso_load(&J->k, b, j, g, c);
+#endif
 #if WSO_MUTANT == 12
                         dkj[c] += ds * wso_load(&J->q, b, i, h, c);
 #else
                         dkj[c] += J->scale * ds * wso_load(&J->q, b, i, h, c);
 #endif
+#if WSO_MUTANT == 15
+                        dvj[c] += p[j] * l * wso_load(&dov, b, i, h, c);
+#else
                         dvj[c] += p[j] * wso_load(&dov, b, i, h, c);
+#endif
                     }
                 }
             }

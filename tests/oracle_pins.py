@@ -599,4 +599,7 @@ MUTANTS = {
     11: "gradient: D_i term dropped from dS",
     12: "gradient: scale dropped from dK",
     13: "first padding token of a short new block used as a key",
+    14: "gradient: dQ sums the values instead of the keys",
+    15: "gradient: dV weighted by the unnormalised weights",
+    16: "gradient: D_i sums dP without the softmax weights",
 }
