@@ -182,3 +182,31 @@ def test_bwd_full_size_elementwise():
     idx = torch.from_numpy(rows).to(dq.device)
     sel = dq[idx[:, 0], idx[:, 2], idx[:, 1]].float().cpu().numpy().astype(np.float64)
     _compare("dq rows", sel, want)
+
+
+def _draw_grad_case(seed):
+    """A seeded random shape: GQA ratio 1, 2, 3, 4 or 8 over 1-4 KV heads,
+    head dim 64 or 128, 1-2 streams, 1-700 tokens in up to 20 blocks (empty
+    blocks included), token-causal segments in some."""
+    g = np.random.default_rng([seed, 2026])
+    Hkv = int(g.integers(1, 5))
+    Hq = Hkv * int(g.choice([1, 2, 3, 4, 8]))
+    D = int(g.choice([64, 128]))
+    B = int(g.integers(1, 3))
+    L = int(g.integers(1, 701))
+    nb = int(g.integers(1, min(L, 20) + 1))
+    lens = []
+    for _ in range(B):
+        cuts = np.sort(g.integers(0, L + 1, size=nb - 1))   # repeated cuts give empty blocks
+        lens.append(np.diff(np.concatenate([[0], cuts, [L]])))
+    text = None
+    if g.random() < 0.4:
+        off = np.stack([np.concatenate([[0], np.cumsum(bl)]) for bl in lens]).astype(np.int64)
+        text = np.array([[g.integers(off[b, n], off[b, n + 1] + 1) for n in range(nb)] for b in range(B)],
+                        np.int32)
+    return _grad_case(f"bwd_rand_{seed}", B, Hq, Hkv, D, lens, seed=3000 + seed, text=text)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_bwd_random_shapes(seed):
+    _check(*_draw_grad_case(seed))
