@@ -60,17 +60,44 @@ def _real(t, n_real, tok_dim):
 def test_solver_loop_graph_replays_match_eager(mode):
     """performer: plain blocks; thinker: token-causal segments; mixed: new
     blocks of 48 and 21 tokens padded to 48, with segments."""
-    B, Hq, Hkv, D, Lq, lens = 2, 8, 2, 128, 48, [700, 333]
-    wl = inputs.step_workload("graph_loop", B, Hq, Hkv, D, Lq, lens, seed=71)
+    starts = {"performer": None, "thinker": [0, 20], "mixed": [40, 5]}[mode]
+    n_real = [48, 21] if mode == "mixed" else None
+    _check_graph_loop(2, 8, 2, 128, 48, [700, 333], 71, starts, n_real, mode)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_graph_replays_random_shapes(seed):
+    """The same loop on seeded random shapes: GQA ratio 1-8 over 1-3 KV
+    heads, head dim 64 or 128, 1-3 streams, blocks of 1-200 tokens over
+    caches of 0-4000 (empty ones included), segments and blocks of
+    different lengths in some."""
+    g = np.random.default_rng([seed, 2028])
+    Hkv = int(g.integers(1, 4))
+    Hq = Hkv * int(g.choice([1, 2, 3, 4, 8]))
+    D = int(g.choice([64, 128]))
+    B = int(g.integers(1, 4))
+    Lq = int(g.integers(1, 201))
+    lens = [int(x) for x in g.integers(0, 4001, size=B)]
+    if g.random() < 0.3:
+        lens[int(g.integers(0, B))] = 0
+    starts = [int(x) for x in g.integers(0, Lq + 1, size=B)] if g.random() < 0.4 else None
+    n_real = [int(x) for x in g.integers(1, Lq + 1, size=B)] if g.random() < 0.3 and Lq > 1 else None
+    _check_graph_loop(B, Hq, Hkv, D, Lq, lens, 7100 + seed, starts, n_real, f"random {seed}")
+
+
+def _check_graph_loop(B, Hq, Hkv, D, Lq, lens, seed, starts, n_real, tag):
+    """Eager loop against the oracle, then three replays of the captured
+    loop (eager work and synchronisations in between), each bitwise the
+    eager results: outputs, lse and the pool after the commit."""
+    wl = inputs.step_workload("graph_loop", B, Hq, Hkv, D, Lq, lens, seed=seed)
     cache = gs.device_cache(wl, wl.cache_lens)
     k0, v0 = cache.k_pool.clone(), cache.v_pool.clone()
     lens_p = _pair(wl.cache_lens)
-    starts = {"performer": None, "thinker": [0, 20], "mixed": [40, 5]}[mode]
-    n_real = [48, 21] if mode == "mixed" else None
     text = _pair(np.array(starts)) if starts is not None else None
     nl = _pair(np.array(n_real)) if n_real is not None else None
     bufs = _loop_buffers(wl, 4, n_real)
-    gs.say(f"[gpu] solver loop eager, {mode}")
+    gs.say(f"[gpu] solver loop eager, {tag}: B={B} Hq={Hq} Hkv={Hkv} D={D} Lq={Lq} cache={lens} "
+           f"starts={starts} new_lens={n_real}")
     _run_loop(cache, lens_p, text, bufs, nl)
     torch.cuda.synchronize()
     ref = [_real(o, n_real, 1).clone() for o in bufs[3]] + [_real(l, n_real, 2).clone() for l in bufs[4]]

@@ -15,14 +15,14 @@ from tests import gpu_support as gs
 pytestmark = pytest.mark.gpu
 
 
-def _case(name, B, Hq, Hkv, Lq, lens, seed):
-    wl = inputs.step_workload(name, B, Hq, Hkv, 128, Lq, lens, seed=seed)
+def _case(name, B, Hq, Hkv, Lq, lens, seed, D=128):
+    wl = inputs.step_workload(name, B, Hq, Hkv, D, Lq, lens, seed=seed)
     cache = gs.device_cache(wl, wl.cache_lens)
     dev = gs.dev()
     lens_h = torch.from_numpy(wl.cache_lens.astype(np.int32))
     bufs = dict(q=gs.to_dev_bf16(wl.q), k=gs.to_dev_bf16(wl.k_new), v=gs.to_dev_bf16(wl.v_new),
                 lens=(lens_h, lens_h.to(dev)),
-                out=torch.full((B, Lq, Hq, 128), float("nan"), dtype=torch.bfloat16, device=dev),
+                out=torch.full((B, Lq, Hq, D), float("nan"), dtype=torch.bfloat16, device=dev),
                 lse=torch.full((B, Hq, Lq), float("nan"), dtype=torch.float32, device=dev))
     return wl, cache, bufs
 
@@ -65,6 +65,30 @@ def test_noalloc_matches_workspace_entry_point_twice():
     # and both agree with the oracle within the output tolerance
     ref, ref_lse = gs.run_oracle(wl2)
     gs.assert_close(gs.compare(o2, l2, ref, ref_lse))
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_noalloc_random_shapes_match_workspace_entry_point(seed):
+    """Seeded random steps (GQA ratio 1-8, head dim 64 or 128, 1-3 streams,
+    blocks of 1-300 tokens over caches of 0-6000, so the split count varies
+    from call to call on the shared scratch array), each bitwise the
+    workspace entry point's result."""
+    g = np.random.default_rng([seed, 2027])
+    Hkv = int(g.integers(1, 4))
+    Hq = Hkv * int(g.choice([1, 2, 3, 4, 8]))
+    D = int(g.choice([64, 128]))
+    B = int(g.integers(1, 4))
+    Lq = int(g.integers(1, 301))
+    lens = [int(x) for x in g.integers(0, 6001, size=B)]
+    ns, need = ws.step_plan(B, Hq, Hkv, Lq, np.asarray(lens, np.int32))
+    assert need <= ws.NOALLOC_SCRATCH_BYTES
+    wl, cache, b = _case(f"noalloc_rand_{seed}", B, Hq, Hkv, Lq, lens, seed=600 + seed, D=D)
+    gs.say(f"[gpu] {wl.name}: B={B} Hq={Hq} Hkv={Hkv} D={D} Lq={Lq} cache={lens}, {ns} splits")
+    o, l = _noalloc(wl, cache, b)
+    r, rl = _reference(wl, cache, b)
+    torch.cuda.synchronize()
+    assert torch.equal(o.view(torch.int16), r.view(torch.int16))
+    assert torch.equal(l.view(torch.int32), rl.view(torch.int32))
 
 
 def test_noalloc_rejects_steps_beyond_its_scratch():
