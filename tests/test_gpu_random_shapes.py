@@ -111,3 +111,28 @@ def test_random_step_shapes(seed):
             oracle.kv_append(pk, pv, wl.page_table[b:b + 1], wl.cache_lens[b:b + 1], kb[b:b + 1, :n], vb[b:b + 1, :n])
         assert np.array_equal(cache.k_pool.view(torch.int16).cpu().numpy().view(np.uint16), pk)
         assert np.array_equal(cache.v_pool.view(torch.int16).cpu().numpy().view(np.uint16), pv)
+
+
+@pytest.mark.parametrize("Hq,Hkv,D", [(16, 1, 128), (32, 2, 64), (64, 1, 128)])
+def test_large_gqa_ratio_step_and_prefill(Hq, Hkv, D):
+    """GQA ratios of 16, 32 and 64: a step packs (token, query head) rows of
+    a KV group into 256-row tiles (64 heads fill a tile with 4 tokens), the
+    prefill runs one query head per work item; full outputs against the
+    oracle, and the step split across KV tiles."""
+    g = np.random.default_rng([Hq, D, 2029])
+    wl = inputs.step_workload(f"gqa{Hq // Hkv}_step", 2, Hq, Hkv, D, 37, [1500, 3100], seed=Hq + D)
+    cache = gs.device_cache(wl, wl.cache_lens)
+    gs.say(_describe(wl))
+    out, lse = gs.run_gpu(wl, cache=cache)
+    torch.cuda.synchronize()
+    ref, ref_lse = gs.run_oracle(wl)
+    gs.assert_close(gs.compare(out, lse, ref, ref_lse))
+    L = 400
+    cuts = np.sort(g.choice(np.arange(1, L), size=5, replace=False))
+    lens = [np.diff(np.concatenate([[0], cuts, [L]]))]
+    wp = inputs.prefill_workload(f"gqa{Hq // Hkv}_prefill", 1, Hq, Hkv, D, lens, seed=Hq + D + 1)
+    gs.say(_describe(wp))
+    out, lse = gs.run_gpu(wp)
+    torch.cuda.synchronize()
+    ref, ref_lse = gs.run_oracle(wp)
+    gs.assert_close(gs.compare(out, lse, ref, ref_lse))
