@@ -244,6 +244,23 @@ def test_long_split_reads_page_ids_from_memory():
     _covered(wl, cache, rows)
 
 
+def test_million_token_cache():
+    """One stream over 1048576 cached tokens (16384 shuffled pages, 512 MiB
+    of K/V), 8 query heads on one KV head, a 16-token block committed in the
+    same launch: positions, page indices and tile counts at that scale, the
+    keys split across up to 32 work-groups.  Every output and lse against
+    the oracle."""
+    n = 1 << 20
+    wl = inputs.step_workload("step_b1_gqa8x1_q16_c1048576", 1, 8, 1, 128, 16, [n], seed=79, fuse_append=True)
+    ns, _ = ws.step_plan(1, 8, 1, 16, wl.cache_lens)
+    cache = gs.device_cache(wl, wl.cache_lens, fill_on_gpu=True)
+    gs.say(f"[gpu] {wl.name}: {ns} splits")
+    out, lse = gs.run_gpu(wl, cache=cache)
+    torch.cuda.synchronize()
+    ref, ref_lse = gs.run_oracle(wl)
+    gs.assert_close(gs.compare(out, lse, ref, ref_lse))
+
+
 def test_device_plan_matches_its_compute_units():
     """Steps are planned for the compute units the device reports."""
     cus = torch.cuda.get_device_properties(0).multi_processor_count
