@@ -48,7 +48,9 @@
  * - All device pointers are HIP device memory of the current device; the
  *   caller owns every buffer (inputs, outputs, cache pool, page tables,
  *   workspace).  The library allocates no device memory and keeps no state
- *   between calls except its loaded code object.
+ *   between calls except its loaded code object (which holds the scratch
+ *   array of ws_block_causal_attn_fwd_noalloc) and, per device, the
+ *   compute-unit count and that array's address, looked up once.
  * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
  *   All device work is enqueued on it; the call returns after enqueueing
  *   (stream-ordered, asynchronous).  Host arrays are read only during the
